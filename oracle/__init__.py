@@ -1,0 +1,198 @@
+"""CPU oracle for the Prox sparse SwiGLU FFN decode step.
+
+TEST INFRASTRUCTURE ONLY.  The oracle is the plain fp64 reference that the
+HIP path is checked against.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import it; the product package never does.
+
+The arithmetic lives in ``oracle.c`` (plain C, binary64, no FMA contraction);
+this module only builds it with gcc and marshals numpy arrays through ctypes.
+Each wrapper names the passage of the paper its C function follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+PROXY_QUANT = 0   # W~ from codes/scales
+PROXY_NONE = 1    # W~ = W (unquantised proxy)
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` into ``liboracle.so`` with gcc (OpenMP, -O2)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+               "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        L = ctypes.CDLL(_LIB)
+        P, I, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
+        L.oracle_half_to_double.argtypes = [ctypes.c_uint16, I]
+        L.oracle_half_to_double.restype = D
+        L.oracle_double_to_f16.argtypes = [D]
+        L.oracle_double_to_f16.restype = ctypes.c_uint16
+        L.oracle_quantize.argtypes = [P, I, I, I, I, I, P, P]
+        L.oracle_topk.argtypes = [P, I, I, P]
+        L.oracle_select_inputs.argtypes = [P, I, I, I, I, P]
+        L.oracle_proxy.argtypes = [P, I, I, I, I, P, I, I, P, P, P, P, I, P, P, P, P, P, P]
+        L.oracle_select_channels.argtypes = [P, I, I, P]
+        L.oracle_stage2.argtypes = [P, I, I, I, I, P, P, P, P, I, P, P]
+        L.oracle_ffn_dense.argtypes = [P, I, I, I, I, P, P, P, P]
+        L.oracle_ffn_sparse.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, I, I,
+                                        P, P, P, P, P]
+        L.oracle_add_rmsnorm.argtypes = [P, P, I, I, I, D, P]
+        L.oracle_max_threads.restype = I
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _u16(a):
+    return np.ascontiguousarray(a, dtype=np.uint16)
+
+
+def half_to_double(bits: int, dtype: int) -> float:
+    return lib().oracle_half_to_double(int(bits), int(dtype))
+
+
+def double_to_f16(v: float) -> int:
+    """IEEE binary16 round-to-nearest-even of a double (bit pattern)."""
+    return int(lib().oracle_double_to_f16(float(v)))
+
+
+def quantize(w, dtype: int, bits: int, group: int):
+    """Sec. 4.3 symmetric proxy quantisation of a channel-major [f][d] matrix.
+    Returns (codes int8 [f][d], scales fp16-bits uint16 [f][d/group])."""
+    w = _u16(w)
+    f, d = w.shape
+    assert d % group == 0
+    codes = np.empty((f, d), np.int8)
+    scales = np.empty((f, d // group), np.uint16)
+    lib().oracle_quantize(_p(w), dtype, d, f, bits, group, _p(codes), _p(scales))
+    return codes, scales
+
+
+def topk(key, k: int):
+    """App. A.6 top-k: ascending indices of the k largest keys, ties to the lower index."""
+    key = np.ascontiguousarray(key, dtype=np.float64)
+    out = np.empty(k, np.int32)
+    lib().oracle_topk(_p(key), key.size, k, _p(out))
+    return out
+
+
+def select_inputs(x, dtype: int, k_in: int):
+    """Sec. 4.1 input mask as top-k over a_i = max_b |x_{b,i}|; x is [B][d]."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    out = np.empty(k_in, np.int32)
+    lib().oracle_select_inputs(_p(x), dtype, B, d, k_in, _p(out))
+    return out
+
+
+def proxy(x, dtype: int, in_idx, *, codes_g=None, scales_g=None, codes_u=None,
+          scales_u=None, group: int = 0, w_gate=None, w_up=None, kind=PROXY_QUANT):
+    """Sec. 4.1 Stage 1: returns (g~ [B][f], u~ [B][f], s~ [B][f], score [f])."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    in_idx = np.ascontiguousarray(in_idx, dtype=np.int32)
+    if kind == PROXY_QUANT:
+        codes_g = np.ascontiguousarray(codes_g, np.int8)
+        codes_u = np.ascontiguousarray(codes_u, np.int8)
+        scales_g, scales_u = _u16(scales_g), _u16(scales_u)
+        f = codes_g.shape[0]
+    else:
+        w_gate, w_up = _u16(w_gate), _u16(w_up)
+        f = w_gate.shape[0]
+    gt = np.empty((B, f)); ut = np.empty((B, f)); st = np.empty((B, f)); sc = np.empty(f)
+    lib().oracle_proxy(_p(x), dtype, B, d, f, _p(in_idx), in_idx.size, kind,
+                       _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
+                       _p(w_gate), _p(w_up), _p(gt), _p(ut), _p(st), _p(sc))
+    return gt, ut, st, sc
+
+
+def select_channels(score, k_ff: int):
+    """Sec. 4.1 channel mask as top-k over the proxy score."""
+    return topk(score, k_ff)
+
+
+def stage2(x, dtype: int, w_gate, w_up, w_down, ff_idx):
+    """Sec. 4.1 Stage 2 on channels ff_idx: returns (s [B][k_ff], y [B][d])."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    wg, wu, wd = _u16(w_gate), _u16(w_up), _u16(w_down)
+    f = wg.shape[0]
+    ff_idx = np.ascontiguousarray(ff_idx, dtype=np.int32)
+    s = np.empty((B, max(ff_idx.size, 1)))
+    y = np.empty((B, d))
+    lib().oracle_stage2(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), _p(ff_idx),
+                        ff_idx.size, _p(s), _p(y))
+    return s[:, :ff_idx.size], y
+
+
+def ffn_dense(x, dtype: int, w_gate, w_up, w_down):
+    """Sec. 2.1 dense SwiGLU FFN in fp64: y [B][d]."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    wg, wu, wd = _u16(w_gate), _u16(w_up), _u16(w_down)
+    y = np.empty((B, d))
+    lib().oracle_ffn_dense(_p(x), dtype, B, d, wg.shape[0], _p(wg), _p(wu), _p(wd), _p(y))
+    return y
+
+
+def ffn_sparse(x, dtype: int, w_gate, w_up, w_down, k_in: int, k_ff: int, *,
+               codes_g=None, scales_g=None, codes_u=None, scales_u=None, group: int = 0,
+               kind=PROXY_QUANT, mask_override=None):
+    """Whole Sec. 4.1 decode step.  Returns dict(y, in_idx, score, ff_idx)."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    wg, wu, wd = _u16(w_gate), _u16(w_up), _u16(w_down)
+    f = wg.shape[0]
+    if kind == PROXY_QUANT:
+        codes_g = np.ascontiguousarray(codes_g, np.int8)
+        codes_u = np.ascontiguousarray(codes_u, np.int8)
+        scales_g, scales_u = _u16(scales_g), _u16(scales_u)
+    mo = None if mask_override is None else np.ascontiguousarray(mask_override, np.int32)
+    if mo is not None:
+        assert mo.size == k_ff
+    in_idx = np.empty(k_in, np.int32)
+    score = np.empty(f)
+    ff_idx = np.empty(k_ff, np.int32)
+    y = np.empty((B, d))
+    lib().oracle_ffn_sparse(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), kind,
+                            _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
+                            k_in, k_ff, _p(mo), _p(in_idx), _p(score), _p(ff_idx), _p(y))
+    return {"y": y, "in_idx": in_idx, "score": score, "ff_idx": ff_idx}
+
+
+def add_rmsnorm(x, y, dtype: int, eps: float = 1e-6):
+    """Residual add then unit-gain RMSNorm between stacked layers, fp64."""
+    x = _u16(np.atleast_2d(x)); y = _u16(np.atleast_2d(y))
+    B, d = x.shape
+    out = np.empty((B, d))
+    lib().oracle_add_rmsnorm(_p(x), _p(y), dtype, B, d, float(eps), _p(out))
+    return out
+
+
+def max_threads() -> int:
+    return int(lib().oracle_max_threads())

@@ -1,0 +1,421 @@
+/*
+ * oracle.c -- plain CPU oracle for the Prox sparse SwiGLU FFN decode step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is the slow, obviously-correct reference
+ * that the HIP path is checked against.  Only the test suite, the smoke check
+ * and the benchmark's CPU-baseline leg may load it; the product library never
+ * does, and this file shares no code, header or table with it.
+ *
+ * Arithmetic is IEEE binary64 throughout.  16-bit inputs (bf16 or fp16 bit
+ * patterns) are converted to double exactly.  The file is compiled with
+ * -ffp-contract=off so no multiply-add is fused.  OpenMP only splits
+ * independent output channels / columns across threads; every individual sum
+ * is taken in the ascending index order written below.
+ *
+ * Notation (Sec. 2.1): W_gate, W_up in R^{d x f}; W_down in R^{f x d};
+ * u = x W_up, h = SiLU(x W_gate), s = u (.) h.  Storage is channel-major:
+ *   wg[j*d + i] = W_gate[i, j],  wu[j*d + i] = W_up[i, j],
+ *   wd[j*d + c] = W_down[j, c];  x[b*d + i] for batch row b.
+ * Proxy codes use the same [f][d] layout; scales are [f][d/group].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define DT_F16 0
+#define DT_BF16 1
+
+/* ------------------------------------------------------------------ */
+/* Exact 16-bit -> double conversions, and double -> fp16 rounding      */
+/* ------------------------------------------------------------------ */
+
+static double bf16_to_double(uint16_t h)
+{
+    /* bf16 is the top half of an IEEE binary32. */
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static double f16_to_double(uint16_t h)
+{
+    /* IEEE binary16: 1 sign, 5 exponent (bias 15), 10 fraction bits. */
+    int sign = h >> 15, e = (h >> 10) & 31, m = h & 1023;
+    double v;
+    if (e == 0)
+        v = ldexp((double)m, -24);               /* subnormal: m * 2^-24 */
+    else if (e == 31)
+        v = m ? NAN : INFINITY;
+    else
+        v = ldexp((double)(m + 1024), e - 25);   /* (1 + m/1024) * 2^(e-15) */
+    return sign ? -v : v;
+}
+
+double oracle_half_to_double(uint16_t h, int dtype)
+{
+    return dtype == DT_BF16 ? bf16_to_double(h) : f16_to_double(h);
+}
+
+/* Round a double to IEEE binary16, round-to-nearest ties-to-even. */
+uint16_t oracle_double_to_f16(double v)
+{
+    uint16_t sign = signbit(v) ? 0x8000 : 0;
+    double a = fabs(v);
+    if (isnan(v))
+        return 0x7E00;
+    if (a == 0.0)
+        return sign;
+    int e2;
+    frexp(a, &e2);                 /* a in [2^(e2-1), 2^e2) */
+    int E = e2 - 1;                /* unbiased exponent of a */
+    if (E < -14)
+        E = -14;                   /* subnormal binade shares the 2^-24 quantum */
+    double quantum = ldexp(1.0, E - 10);
+    double r = nearbyint(a / quantum) * quantum;   /* default mode: ties to even */
+    if (r >= 65536.0)
+        return sign | 0x7C00;      /* overflow to infinity */
+    if (r < ldexp(1.0, -14))
+        return sign | (uint16_t)(r / ldexp(1.0, -24));
+    int er;
+    double fr = frexp(r, &er);     /* r = fr * 2^er, fr in [0.5, 1) */
+    uint16_t biased = (uint16_t)(er - 1 + 15);
+    uint16_t mant = (uint16_t)((fr * 2.0 - 1.0) * 1024.0);
+    return sign | (uint16_t)(biased << 10) | mant;
+}
+
+static double silu(double z)
+{
+    /* SiLU(z) = z * sigmoid(z) = z / (1 + e^{-z})  (Sec. 2.1). */
+    return z / (1.0 + exp(-z));
+}
+
+#define XV(b, i) oracle_half_to_double(x[(size_t)(b) * d + (i)], dtype)
+#define WV(w, j, i) oracle_half_to_double((w)[(size_t)(j) * d + (i)], dtype)
+
+/* ------------------------------------------------------------------ */
+/* Step 1 -- proxy quantisation (Sec. 4.3)                              */
+/* ------------------------------------------------------------------ */
+/*
+ * Symmetric quantisation of one matrix W (channel-major [f][d]).  For each
+ * output channel j and each group of `group` consecutive input channels:
+ *   amax  = max |W[i,j]| over the group
+ *   sigma = fp16_RNE(amax / qmax),  qmax = 2^(bits-1) - 1   (7 or 127)
+ *   q     = clamp(round_half_even(W[i,j] / sigma), -qmax, qmax), q = 0 if sigma == 0
+ * group == d gives one scale per output channel (per-row quantisation).
+ * codes: int8 [f][d]; scales: fp16 bits [f][d/group].
+ */
+void oracle_quantize(const uint16_t *w, int dtype, int d, int f, int bits, int group,
+                     int8_t *codes, uint16_t *scales)
+{
+    const int qmax = (1 << (bits - 1)) - 1;
+    const int ng = d / group;
+#pragma omp parallel for schedule(static)
+    for (int j = 0; j < f; ++j) {
+        for (int g = 0; g < ng; ++g) {
+            double amax = 0.0;
+            for (int i = g * group; i < (g + 1) * group; ++i) {
+                double a = fabs(WV(w, j, i));
+                if (a > amax)
+                    amax = a;
+            }
+            uint16_t sbits = oracle_double_to_f16(amax / (double)qmax);
+            scales[(size_t)j * ng + g] = sbits;
+            double sigma = f16_to_double(sbits);
+            for (int i = g * group; i < (g + 1) * group; ++i) {
+                double q = 0.0;
+                if (sigma != 0.0) {
+                    q = nearbyint(WV(w, j, i) / sigma);
+                    if (q > qmax)
+                        q = qmax;
+                    if (q < -qmax)
+                        q = -qmax;
+                }
+                codes[(size_t)j * d + i] = (int8_t)q;
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Top-k selection (App. A.6, per-token top-k rule)                     */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    double key;
+    int idx;
+} keyed;
+
+static int by_key_desc_then_index(const void *pa, const void *pb)
+{
+    const keyed *a = (const keyed *)pa, *b = (const keyed *)pb;
+    if (a->key > b->key)
+        return -1;
+    if (a->key < b->key)
+        return 1;
+    return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+static int int_asc(const void *pa, const void *pb)
+{
+    int a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    return (a > b) - (a < b);
+}
+
+/* Indices of the k largest keys, ties going to the lower index; the result
+ * is returned in ascending index order. */
+void oracle_topk(const double *key, int n, int k, int32_t *idx_out)
+{
+    keyed *arr = (keyed *)malloc(sizeof(keyed) * (size_t)(n > 0 ? n : 1));
+    for (int i = 0; i < n; ++i) {
+        arr[i].key = key[i];
+        arr[i].idx = i;
+    }
+    qsort(arr, (size_t)n, sizeof(keyed), by_key_desc_then_index);
+    for (int t = 0; t < k; ++t)
+        idx_out[t] = arr[t].idx;
+    qsort(idx_out, (size_t)k, sizeof(int32_t), int_asc);
+    free(arr);
+}
+
+/* Step 2 -- input mask m_x (Sec. 4.1) read as a per-token top-k: keep the
+ * k_in input channels with the largest a_i = max_b |x_{b,i}| (one set shared
+ * by the batch rows). */
+void oracle_select_inputs(const uint16_t *x, int dtype, int B, int d, int k_in,
+                          int32_t *in_idx)
+{
+    double *a = (double *)malloc(sizeof(double) * (size_t)d);
+    for (int i = 0; i < d; ++i) {
+        double m = 0.0;
+        for (int b = 0; b < B; ++b) {
+            double v = fabs(XV(b, i));
+            if (v > m)
+                m = v;
+        }
+        a[i] = m;
+    }
+    oracle_topk(a, d, k_in, in_idx);
+    free(a);
+}
+
+/* ------------------------------------------------------------------ */
+/* Step 3 -- proxy intermediate state (Sec. 4.1, Stage 1)               */
+/* ------------------------------------------------------------------ */
+/*
+ * g~ = Pi_in(x, W~_gate, m_x),  u~ = Pi_in(x, W~_up, m_x),
+ * s~ = SiLU(g~) (.) u~,  score_j = max_b |s~_{b,j}|.
+ * proxy_kind 0: W~[i,j] = q[i,j] * sigma[g(i), j] from codes/scales.
+ * proxy_kind 1: W~ = W itself (unquantised proxy).
+ * gt, ut, st are [B][f] (may be NULL); score is [f].
+ */
+void oracle_proxy(const uint16_t *x, int dtype, int B, int d, int f,
+                  const int32_t *in_idx, int k_in, int proxy_kind,
+                  const int8_t *cg, const uint16_t *sg,
+                  const int8_t *cu, const uint16_t *su, int group,
+                  const uint16_t *wg, const uint16_t *wu,
+                  double *gt, double *ut, double *st, double *score)
+{
+    const int ng = group > 0 ? d / group : 0;
+#pragma omp parallel for schedule(static)
+    for (int j = 0; j < f; ++j) {
+        double best = 0.0;
+        for (int b = 0; b < B; ++b) {
+            double g = 0.0, u = 0.0;
+            for (int t = 0; t < k_in; ++t) {
+                int i = in_idx[t];
+                double xi = XV(b, i), wgt, wut;
+                if (proxy_kind == 0) {
+                    size_t sidx = (size_t)j * ng + i / group;
+                    wgt = (double)cg[(size_t)j * d + i] * f16_to_double(sg[sidx]);
+                    wut = (double)cu[(size_t)j * d + i] * f16_to_double(su[sidx]);
+                } else {
+                    wgt = WV(wg, j, i);
+                    wut = WV(wu, j, i);
+                }
+                g += xi * wgt;
+                u += xi * wut;
+            }
+            double s = silu(g) * u;
+            if (gt)
+                gt[(size_t)b * f + j] = g;
+            if (ut)
+                ut[(size_t)b * f + j] = u;
+            if (st)
+                st[(size_t)b * f + j] = s;
+            if (fabs(s) > best)
+                best = fabs(s);
+        }
+        score[j] = best;
+    }
+}
+
+/* Step 4 -- channel mask m_s (Sec. 4.1) read as top-k over the proxy score,
+ * shared by the batch. */
+void oracle_select_channels(const double *score, int f, int k_ff, int32_t *ff_idx)
+{
+    oracle_topk(score, f, k_ff, ff_idx);
+}
+
+/* ------------------------------------------------------------------ */
+/* Step 5 -- exact sparse computation (Sec. 4.1, Stage 2)               */
+/* ------------------------------------------------------------------ */
+/*
+ * For the selected channels j (ascending), over ALL d inputs:
+ *   g_j = x . W_gate[:, j],  u_j = x . W_up[:, j],  s_j = SiLU(g_j) u_j
+ *   y   = sum_{j in M, ascending} s_j W_down[j, :]
+ * s_out is [B][k_ff] (may be NULL), y is [B][d].
+ */
+void oracle_stage2(const uint16_t *x, int dtype, int B, int d, int f,
+                   const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
+                   const int32_t *ff_idx, int k_ff, double *s_out, double *y)
+{
+    (void)f;
+    double *s = (double *)malloc(sizeof(double) * (size_t)B * (size_t)(k_ff > 0 ? k_ff : 1));
+#pragma omp parallel for schedule(static)
+    for (int t = 0; t < k_ff; ++t) {
+        int j = ff_idx[t];
+        for (int b = 0; b < B; ++b) {
+            double g = 0.0, u = 0.0;
+            for (int i = 0; i < d; ++i) {
+                double xi = XV(b, i);
+                g += xi * WV(wg, j, i);
+                u += xi * WV(wu, j, i);
+            }
+            s[(size_t)b * k_ff + t] = silu(g) * u;
+        }
+    }
+    const int cblk = 256;
+#pragma omp parallel for schedule(static)
+    for (int c0 = 0; c0 < d; c0 += cblk) {
+        int c1 = c0 + cblk < d ? c0 + cblk : d;
+        for (int b = 0; b < B; ++b) {
+            double *yb = y + (size_t)b * d;
+            for (int c = c0; c < c1; ++c)
+                yb[c] = 0.0;
+            for (int t = 0; t < k_ff; ++t) {
+                int j = ff_idx[t];
+                double sj = s[(size_t)b * k_ff + t];
+                for (int c = c0; c < c1; ++c)
+                    yb[c] += sj * WV(wd, j, c);
+            }
+        }
+    }
+    if (s_out)
+        memcpy(s_out, s, sizeof(double) * (size_t)B * (size_t)k_ff);
+    free(s);
+}
+
+/* ------------------------------------------------------------------ */
+/* Dense SwiGLU FFN (Sec. 2.1): y = (x W_up (.) SiLU(x W_gate)) W_down   */
+/* ------------------------------------------------------------------ */
+void oracle_ffn_dense(const uint16_t *x, int dtype, int B, int d, int f,
+                      const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
+                      double *y)
+{
+    double *s = (double *)malloc(sizeof(double) * (size_t)B * (size_t)f);
+#pragma omp parallel for schedule(static)
+    for (int j = 0; j < f; ++j) {
+        for (int b = 0; b < B; ++b) {
+            double g = 0.0, u = 0.0;
+            for (int i = 0; i < d; ++i) {
+                double xi = XV(b, i);
+                g += xi * WV(wg, j, i);
+                u += xi * WV(wu, j, i);
+            }
+            s[(size_t)b * f + j] = u * silu(g);
+        }
+    }
+    const int cblk = 256;
+#pragma omp parallel for schedule(static)
+    for (int c0 = 0; c0 < d; c0 += cblk) {
+        int c1 = c0 + cblk < d ? c0 + cblk : d;
+        for (int b = 0; b < B; ++b) {
+            double *yb = y + (size_t)b * d;
+            for (int c = c0; c < c1; ++c)
+                yb[c] = 0.0;
+            for (int j = 0; j < f; ++j) {
+                double sj = s[(size_t)b * f + j];
+                for (int c = c0; c < c1; ++c)
+                    yb[c] += sj * WV(wd, j, c);
+            }
+        }
+    }
+    free(s);
+}
+
+/* ------------------------------------------------------------------ */
+/* The whole sparse decode step: Stage 1 then Stage 2 (Sec. 4.1)        */
+/* ------------------------------------------------------------------ */
+/*
+ * mask_override: NULL, or an ascending list of k_ff channels used instead of
+ * the proxy's selection (to evaluate Stage 2 on another implementation's
+ * mask).  Optional outputs (NULL to skip): in_idx_out [k_in], score_out [f],
+ * ff_idx_out [k_ff].  y is [B][d].
+ */
+void oracle_ffn_sparse(const uint16_t *x, int dtype, int B, int d, int f,
+                       const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
+                       int proxy_kind, const int8_t *cg, const uint16_t *sg,
+                       const int8_t *cu, const uint16_t *su, int group,
+                       int k_in, int k_ff, const int32_t *mask_override,
+                       int32_t *in_idx_out, double *score_out, int32_t *ff_idx_out,
+                       double *y)
+{
+    int32_t *in_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)k_in);
+    int32_t *ff_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)k_ff);
+    double *score = (double *)malloc(sizeof(double) * (size_t)f);
+    if (mask_override) {
+        memcpy(ff_idx, mask_override, sizeof(int32_t) * (size_t)k_ff);
+        if (in_idx_out || score_out) {
+            oracle_select_inputs(x, dtype, B, d, k_in, in_idx);
+            oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
+                         wg, wu, NULL, NULL, NULL, score);
+        }
+    } else {
+        oracle_select_inputs(x, dtype, B, d, k_in, in_idx);
+        oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
+                     wg, wu, NULL, NULL, NULL, score);
+        oracle_select_channels(score, f, k_ff, ff_idx);
+    }
+    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y);
+    if (in_idx_out)
+        memcpy(in_idx_out, in_idx, sizeof(int32_t) * (size_t)k_in);
+    if (score_out)
+        memcpy(score_out, score, sizeof(double) * (size_t)f);
+    if (ff_idx_out)
+        memcpy(ff_idx_out, ff_idx, sizeof(int32_t) * (size_t)k_ff);
+    free(in_idx);
+    free(ff_idx);
+    free(score);
+}
+
+/* ------------------------------------------------------------------ */
+/* Residual + RMSNorm between stacked layers (unit gain)                */
+/* ------------------------------------------------------------------ */
+/* out_b = r_b / sqrt(mean(r_b^2) + eps),  r_b = x_b + y_b.  out is [B][d]. */
+void oracle_add_rmsnorm(const uint16_t *x, const uint16_t *y, int dtype, int B, int d,
+                        double eps, double *out)
+{
+    for (int b = 0; b < B; ++b) {
+        double ss = 0.0;
+        for (int i = 0; i < d; ++i) {
+            double r = XV(b, i) + oracle_half_to_double(y[(size_t)b * d + i], dtype);
+            ss += r * r;
+        }
+        double inv = 1.0 / sqrt(ss / d + eps);
+        for (int i = 0; i < d; ++i) {
+            double r = XV(b, i) + oracle_half_to_double(y[(size_t)b * d + i], dtype);
+            out[(size_t)b * d + i] = r * inv;
+        }
+    }
+}
+
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

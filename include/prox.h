@@ -1,0 +1,179 @@
+/*
+ * prox.h -- C-ABI of libprox.so: the Prox sparse SwiGLU FFN decode step
+ * (two-stage, training-free activation sparsity; arxiv 2607.27591) on AMD
+ * MI355X (gfx950).
+ *
+ * Notation follows the paper (Sec. 2.1): W_gate, W_up in R^{d x f},
+ * W_down in R^{f x d}, u = x W_up, h = SiLU(x W_gate), s = u (.) h.
+ * d = d_model, f = d_ff, B = batch rows decoded together.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers named as device pointers must point to device memory that the
+ *    caller allocated and owns; the library never allocates, frees or
+ *    synchronises inside prox_ffn_* / prox_pack_proxy / prox_add_rmsnorm.
+ *    All work is enqueued on the given HIP stream (0 = the null stream) and
+ *    completes asynchronously.
+ *  - Arguments are validated on the host before any HIP call; on failure
+ *    nothing is enqueued and a status other than PROX_OK is returned.  No
+ *    entry point aborts or throws.
+ *  - Calls are reentrant when they use distinct workspaces.  Two calls that
+ *    share a workspace must be ordered on one stream.
+ *  - 16-bit tensors are IEEE fp16 or bf16 bit patterns (prox_dtype).  Inputs
+ *    must be finite.
+ */
+#ifndef PROX_H
+#define PROX_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PROX_OK = 0,
+    PROX_ERR_INVALID = 1,     /* null pointer, size out of range, misalignment */
+    PROX_ERR_UNSUPPORTED = 2, /* well-formed but outside the supported shapes */
+    PROX_ERR_WORKSPACE = 3,   /* workspace (or proxy blob) smaller than required */
+    PROX_ERR_HIP = 4          /* a HIP launch or runtime call failed */
+} prox_status;
+
+typedef enum { PROX_F16 = 0, PROX_BF16 = 1 } prox_dtype;
+
+typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1 } prox_qfmt;
+
+/* Supported sizes. */
+#define PROX_MAX_BATCH 16
+#define PROX_MIN_D_MODEL 128
+#define PROX_MAX_D_MODEL 16384   /* multiple of 128 */
+#define PROX_MAX_D_FF 65536
+#define PROX_SPARSE_STAGES 5     /* events recorded by prox_ffn_sparse_staged */
+
+/*
+ * Original FFN weights (Sec. 2.1), all three channel-major: row j holds the
+ * d entries that meet intermediate channel j, so a kept channel reads three
+ * contiguous rows.
+ *   w_gate[j*d + i] = W_gate[i, j]   (nn.Linear gate_proj.weight)
+ *   w_up  [j*d + i] = W_up[i, j]     (nn.Linear up_proj.weight)
+ *   w_down[j*d + c] = W_down[j, c]   (nn.Linear down_proj.weight, transposed)
+ * Device pointers, 16-byte aligned, read-only, owned by the caller.
+ */
+typedef struct {
+    int d_model;
+    int d_ff;
+    prox_dtype dtype;
+    const void *w_gate;
+    const void *w_up;
+    const void *w_down;
+} prox_weights;
+
+/*
+ * Quantised proxy copies W~_gate, W~_up of Stage 1 (Sec. 4.3): symmetric
+ * quantisation, one fp16 scale per (output channel, group of `group`
+ * consecutive input channels); group == d_model is one scale per channel.
+ *   sigma = fp16_RNE(amax / qmax), q = clamp(round_half_even(w / sigma),
+ *   -qmax, qmax), qmax = 7 (INT4) or 127 (INT8), q = 0 when sigma == 0.
+ * `blob` is an opaque, device-resident, caller-allocated buffer of at least
+ * prox_proxy_bytes() bytes (16-byte aligned).  It starts with a 256-byte
+ * header (magic "PRXB", version, fmt, group, d_model, d_ff, tile width) so a
+ * saved blob describes itself.  group must be a multiple of 128 dividing
+ * d_model.
+ */
+typedef struct {
+    prox_qfmt fmt;
+    int group;
+    void *blob;
+    size_t bytes;
+} prox_proxy;
+
+/* Bytes of the proxy blob for this shape; 0 if the shape is unsupported. */
+size_t prox_proxy_bytes(int d_model, int d_ff, prox_qfmt fmt, int group);
+
+/*
+ * Offline preparation (Sec. 4.3): quantise w->w_gate and w->w_up into
+ * p->blob.  Bit-exact and deterministic.  p->fmt, p->group, p->blob and
+ * p->bytes are inputs.
+ */
+prox_status prox_pack_proxy(const prox_weights *w, prox_proxy *p, hipStream_t stream);
+
+/*
+ * Inverse view of a packed blob, for inspection and tests: writes the integer
+ * codes q (int8, [d_ff][d_model], channel-major like the weights) and the
+ * fp16 scale bit patterns ([d_ff][d_model/group]) of both proxies.  All four
+ * outputs are device pointers.
+ */
+prox_status prox_unpack_proxy(const prox_proxy *p, int d_model, int d_ff, int8_t *codes_gate,
+                              uint16_t *scales_gate, int8_t *codes_up, uint16_t *scales_up,
+                              hipStream_t stream);
+
+/* Workspace bytes needed by prox_ffn_sparse / prox_ffn_dense for this shape
+ * and batch; 0 if unsupported.  The workspace needs no initialisation. */
+size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
+
+/*
+ * Dense SwiGLU FFN (Sec. 2.1):  y = (x W_up (.) SiLU(x W_gate)) W_down.
+ *   x: device [batch][d_model], w->dtype;  y: device [batch][d_model], same
+ *   dtype, rounded once (round-to-nearest-even) from fp32 accumulation.
+ *   ws: device workspace of ws_bytes >= prox_workspace_bytes(), 256-byte
+ *   aligned.  1 <= batch <= PROX_MAX_BATCH.
+ */
+prox_status prox_ffn_dense(const prox_weights *w, const void *x, int batch, void *y, void *ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The Prox sparse decode step (Sec. 4.1), with the per-token top-k rule of
+ * App. A.6 for both masks:
+ *  Stage 1  m_x = the k_in input channels with the largest a_i = max_b |x_{b,i}|
+ *           (one set shared by the batch; ties go to the lower index);
+ *           g~ = Pi_in(x, W~_gate, m_x), u~ = Pi_in(x, W~_up, m_x) in fp32;
+ *           score_j = max_b |SiLU(g~_{b,j}) u~_{b,j}|;
+ *           m_s = the k_ff channels with the largest score (ties to the lower
+ *           index), shared by the batch.
+ *  Stage 2  for j in m_s, over all d inputs: g_j, u_j exact (fp32 accumulation
+ *           of the original weights), s_j = SiLU(g_j) u_j kept in fp32;
+ *           y = sum_{j in m_s} s_j W_down[j, :], rounded once to the dtype.
+ * Arguments:
+ *   x      device [batch][d_model] (w->dtype), 16-byte aligned
+ *   y      device [batch][d_model] output (w->dtype), 16-byte aligned
+ *   mask   device uint8 [d_ff] output: 1 for channels in m_s, else 0
+ *   in_mask  device uint8 [d_model] output for m_x, or NULL
+ *   scores device float [d_ff] output of score_j, or NULL
+ *   1 <= k_in <= d_model, 1 <= k_ff <= d_ff, 1 <= batch <= PROX_MAX_BATCH.
+ */
+prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
+                            int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
+                            float *scores, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * prox_ffn_sparse with timing: `events` holds PROX_SPARSE_STAGES + 1 caller-
+ * created HIP events, recorded on `stream` before the first stage and after
+ * each stage (input select, proxy GEMV + score, channel select, gate/up,
+ * down + output).  Same kernels and launch configuration as prox_ffn_sparse.
+ */
+prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, const void *x,
+                                   int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                                   uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                                   hipEvent_t *events, hipStream_t stream);
+
+/* Name of stage i of prox_ffn_sparse_staged (static string), or NULL. */
+const char *prox_sparse_stage_name(int i);
+
+/*
+ * Residual + unit-gain RMSNorm between stacked FFN layers:
+ *   out_b = r_b / sqrt(mean(r_b^2) + eps),  r_b = x_b + y_b  (fp32),
+ * rounded once to the dtype.  x, y, out: device [batch][d_model]; out may
+ * alias x.
+ */
+prox_status prox_add_rmsnorm(const void *x, const void *y, int batch, int d_model,
+                             prox_dtype dtype, float eps, void *out, hipStream_t stream);
+
+/* Static description of a status code. */
+const char *prox_strerror(prox_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PROX_H */

@@ -1,0 +1,220 @@
+// C-ABI of libprox (declared in include/prox.h): argument validation on the
+// host, workspace carving, and the launch sequence of each entry point.
+#include <prox.h>
+
+#include "kernels.hpp"
+
+using namespace prox;
+
+namespace {
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+bool dtype_ok(int dt) { return dt == PROX_F16 || dt == PROX_BF16; }
+
+bool shape_ok(int d, int f) {
+    return d >= PROX_MIN_D_MODEL && d <= PROX_MAX_D_MODEL && d % 128 == 0 && f >= 1 &&
+           f <= PROX_MAX_D_FF;
+}
+
+int qbits_of(int fmt) { return fmt == PROX_Q_INT4 ? 4 : fmt == PROX_Q_INT8 ? 8 : 0; }
+
+bool proxy_shape_ok(int d, int fmt, int group) {
+    return qbits_of(fmt) != 0 && group >= 128 && group % 128 == 0 && d % group == 0;
+}
+
+prox_status check_weights(const prox_weights *w) {
+    if (!w || !w->w_gate || !w->w_up || !w->w_down) return PROX_ERR_INVALID;
+    if (!dtype_ok(w->dtype)) return PROX_ERR_INVALID;
+    if (!aligned(w->w_gate, 16) || !aligned(w->w_up, 16) || !aligned(w->w_down, 16))
+        return PROX_ERR_INVALID;
+    if (w->d_model < 1 || w->d_ff < 1) return PROX_ERR_INVALID;
+    if (!shape_ok(w->d_model, w->d_ff)) return PROX_ERR_UNSUPPORTED;
+    return PROX_OK;
+}
+
+prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_ERR_HIP; }
+
+#define PROX_TRY(expr)                                \
+    do {                                              \
+        prox_status st_ = hip_status(expr);           \
+        if (st_ != PROX_OK) return st_;               \
+    } while (0)
+
+struct Ws {
+    Ctrl *ctrl;
+    float *proxy_part, *scores, *s, *down_part;
+    int *ff_idx;
+};
+
+Ws carve(void *ws, int d, int f, int batch) {
+    const WsLayout L(d, f, batch);
+    char *b = static_cast<char *>(ws);
+    Ws w;
+    w.ctrl = reinterpret_cast<Ctrl *>(b + L.ctrl);
+    w.proxy_part = reinterpret_cast<float *>(b + L.proxy_part);
+    w.scores = reinterpret_cast<float *>(b + L.scores);
+    w.ff_idx = reinterpret_cast<int *>(b + L.ff_idx);
+    w.s = reinterpret_cast<float *>(b + L.s);
+    w.down_part = reinterpret_cast<float *>(b + L.down_part);
+    return w;
+}
+
+const char *const kStageNames[PROX_SPARSE_STAGES] = {
+    "select_inputs", "proxy_gemv_score", "select_channels", "stage2_gate_up", "stage2_down"};
+
+prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
+                        int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
+                        float *scores, void *ws, size_t ws_bytes, hipEvent_t *events,
+                        hipStream_t stream) {
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    if (!p || !p->blob || !x || !y || !mask || !ws) return PROX_ERR_INVALID;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(p->blob, 16) || !aligned(ws, 256) ||
+        (scores && !aligned(scores, 4)))
+        return PROX_ERR_INVALID;
+    const int d = w->d_model, f = w->d_ff;
+    if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
+    if (k_in < 1 || k_in > d || k_ff < 1 || k_ff > f) return PROX_ERR_INVALID;
+    if (!proxy_shape_ok(d, p->fmt, p->group)) return PROX_ERR_UNSUPPORTED;
+    const int qbits = qbits_of(p->fmt);
+    if (p->bytes < BlobLayout(d, f, qbits, p->group).total) return PROX_ERR_WORKSPACE;
+    if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
+    if (events)
+        for (int i = 0; i <= PROX_SPARSE_STAGES; ++i)
+            if (!events[i]) return PROX_ERR_INVALID;
+
+    const Ws W = carve(ws, d, f, batch);
+    const int dt = w->dtype;
+    const uint16_t *xb = static_cast<const uint16_t *>(x);
+    auto rec = [&](int i) -> hipError_t {
+        return events ? hipEventRecord(events[i], stream) : hipSuccess;
+    };
+
+    PROX_TRY(rec(0));
+    PROX_TRY(launch_select_inputs(x, batch, d, k_in, W.ctrl, in_mask, stream));
+    PROX_TRY(rec(1));
+    for (int c0 = 0; c0 < batch; c0 += kProxyMaxNB) {
+        const int nb = batch - c0 < kProxyMaxNB ? batch - c0 : kProxyMaxNB;
+        PROX_TRY(launch_proxy(dt, qbits, xb + (size_t)c0 * d, nb, x, batch, d, f, p->group, p->blob,
+                              W.ctrl, W.proxy_part, W.scores, c0 > 0, stream));
+    }
+    PROX_TRY(rec(2));
+    PROX_TRY(launch_select_channels(W.scores, f, k_ff, W.ctrl, mask, W.ff_idx, scores, stream));
+    PROX_TRY(rec(3));
+    for (int c0 = 0; c0 < batch; c0 += kGateUpMaxNB) {
+        const int nb = batch - c0 < kGateUpMaxNB ? batch - c0 : kGateUpMaxNB;
+        PROX_TRY(launch_gateup(dt, xb + (size_t)c0 * d, nb, d, w->w_gate, w->w_up, W.ff_idx, k_ff,
+                               W.s + (size_t)c0 * k_ff, k_ff, nullptr, stream));
+    }
+    PROX_TRY(rec(4));
+    PROX_TRY(launch_down(dt, w->w_down, d, W.ff_idx, k_ff, W.s, k_ff, batch, W.down_part, W.ctrl,
+                         y, stream));
+    PROX_TRY(rec(5));
+    return PROX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *prox_strerror(prox_status s) {
+    switch (s) {
+        case PROX_OK: return "ok";
+        case PROX_ERR_INVALID: return "invalid argument";
+        case PROX_ERR_UNSUPPORTED: return "unsupported shape or format";
+        case PROX_ERR_WORKSPACE: return "workspace or proxy buffer too small";
+        case PROX_ERR_HIP: return "HIP runtime or launch error";
+    }
+    return "unknown status";
+}
+
+const char *prox_sparse_stage_name(int i) {
+    return i >= 0 && i < PROX_SPARSE_STAGES ? kStageNames[i] : nullptr;
+}
+
+size_t prox_proxy_bytes(int d_model, int d_ff, prox_qfmt fmt, int group) {
+    if (!shape_ok(d_model, d_ff) || !proxy_shape_ok(d_model, fmt, group)) return 0;
+    return BlobLayout(d_model, d_ff, qbits_of(fmt), group).total;
+}
+
+size_t prox_workspace_bytes(int d_model, int d_ff, int batch) {
+    if (!shape_ok(d_model, d_ff) || batch < 1 || batch > PROX_MAX_BATCH) return 0;
+    return WsLayout(d_model, d_ff, batch).total;
+}
+
+prox_status prox_pack_proxy(const prox_weights *w, prox_proxy *p, hipStream_t stream) {
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    if (!p || !p->blob || !aligned(p->blob, 16)) return PROX_ERR_INVALID;
+    if (!proxy_shape_ok(w->d_model, p->fmt, p->group)) return PROX_ERR_UNSUPPORTED;
+    const int qbits = qbits_of(p->fmt);
+    if (p->bytes < BlobLayout(w->d_model, w->d_ff, qbits, p->group).total)
+        return PROX_ERR_WORKSPACE;
+    return hip_status(launch_pack(w->dtype, qbits, w->w_gate, w->w_up, w->d_model, w->d_ff,
+                                  p->group, p->blob, stream));
+}
+
+prox_status prox_unpack_proxy(const prox_proxy *p, int d_model, int d_ff, int8_t *codes_gate,
+                              uint16_t *scales_gate, int8_t *codes_up, uint16_t *scales_up,
+                              hipStream_t stream) {
+    if (!p || !p->blob || !codes_gate || !scales_gate || !codes_up || !scales_up)
+        return PROX_ERR_INVALID;
+    if (!aligned(p->blob, 16) || !aligned(scales_gate, 2) || !aligned(scales_up, 2))
+        return PROX_ERR_INVALID;
+    if (!shape_ok(d_model, d_ff) || !proxy_shape_ok(d_model, p->fmt, p->group))
+        return PROX_ERR_UNSUPPORTED;
+    const int qbits = qbits_of(p->fmt);
+    if (p->bytes < BlobLayout(d_model, d_ff, qbits, p->group).total) return PROX_ERR_WORKSPACE;
+    return hip_status(launch_unpack(qbits, p->blob, d_model, d_ff, p->group, codes_gate,
+                                    scales_gate, codes_up, scales_up, stream));
+}
+
+prox_status prox_ffn_dense(const prox_weights *w, const void *x, int batch, void *y, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    if (!x || !y || !ws) return PROX_ERR_INVALID;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 256)) return PROX_ERR_INVALID;
+    if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
+    const int d = w->d_model, f = w->d_ff;
+    if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
+    const Ws W = carve(ws, d, f, batch);
+    const uint16_t *xb = static_cast<const uint16_t *>(x);
+    for (int c0 = 0; c0 < batch; c0 += kGateUpMaxNB) {
+        const int nb = batch - c0 < kGateUpMaxNB ? batch - c0 : kGateUpMaxNB;
+        PROX_TRY(launch_gateup(w->dtype, xb + (size_t)c0 * d, nb, d, w->w_gate, w->w_up, nullptr,
+                               f, W.s + (size_t)c0 * f, f, c0 == 0 ? W.ctrl : nullptr, stream));
+    }
+    PROX_TRY(launch_down(w->dtype, w->w_down, d, nullptr, f, W.s, f, batch, W.down_part, W.ctrl,
+                         y, stream));
+    return PROX_OK;
+}
+
+prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
+                            int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
+                            float *scores, void *ws, size_t ws_bytes, hipStream_t stream) {
+    return sparse_impl(w, p, x, batch, k_in, k_ff, y, mask, in_mask, scores, ws, ws_bytes,
+                       nullptr, stream);
+}
+
+prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, const void *x,
+                                   int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                                   uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                                   hipEvent_t *events, hipStream_t stream) {
+    if (!events) return PROX_ERR_INVALID;
+    return sparse_impl(w, p, x, batch, k_in, k_ff, y, mask, in_mask, scores, ws, ws_bytes, events,
+                       stream);
+}
+
+prox_status prox_add_rmsnorm(const void *x, const void *y, int batch, int d_model,
+                             prox_dtype dtype, float eps, void *out, hipStream_t stream) {
+    if (!x || !y || !out || !dtype_ok(dtype)) return PROX_ERR_INVALID;
+    if (!aligned(x, 2) || !aligned(y, 2) || !aligned(out, 2)) return PROX_ERR_INVALID;
+    if (batch < 1 || batch > PROX_MAX_BATCH || d_model < 1) return PROX_ERR_INVALID;
+    if (d_model > PROX_MAX_D_MODEL) return PROX_ERR_UNSUPPORTED;
+    if (!(eps >= 0.0f)) return PROX_ERR_INVALID;
+    return hip_status(launch_add_rmsnorm(dtype, x, y, batch, d_model, eps, out, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,184 @@
+// Device helpers shared by the gfx950 kernels of libprox: wave64 reductions
+// and scans, a block-wide radix k-th-largest search, ordered compaction and
+// 16-bit float conversions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "layout.hpp"
+
+namespace prox {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------------------
+// 16-bit float conversions (exact widening, round-to-nearest-even narrowing)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float f16_bits_to_float(uint32_t h) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+template <int DT>
+__device__ __forceinline__ float lo_to_float(uint32_t w) {
+    if constexpr (DT == kBF16) return bf16_lo(w);
+    else return f16_bits_to_float(w & 0xFFFFu);
+}
+template <int DT>
+__device__ __forceinline__ float hi_to_float(uint32_t w) {
+    if constexpr (DT == kBF16) return bf16_hi(w);
+    else return f16_bits_to_float(w >> 16);
+}
+template <int DT>
+__device__ __forceinline__ float half_to_float(uint16_t h) {
+    return lo_to_float<DT>((uint32_t)h);
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t float_to_bf16_rne(float v) {
+    uint32_t u = __float_as_uint(v);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+// fp32 -> fp16 bits; the hardware conversion rounds to nearest even.
+__device__ __forceinline__ uint16_t float_to_f16_rne(float v) {
+    return __builtin_bit_cast(uint16_t, (_Float16)v);
+}
+template <int DT>
+__device__ __forceinline__ uint16_t float_to_half(float v) {
+    if constexpr (DT == kBF16) return float_to_bf16_rne(v);
+    else return float_to_f16_rne(v);
+}
+
+// Two-term dot product with fp32 accumulation: a.lo*b.lo + a.hi*b.hi + c.
+template <int DT>
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    if constexpr (DT == kBF16)
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                               __builtin_bit_cast(bf16x2, b), c, false);
+    else
+        return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a), __builtin_bit_cast(f16x2, b),
+                                      c, false);
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (non-temporal hint: weights are read once per call).
+__device__ __forceinline__ uint4 load_stream16(const void *p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// ---------------------------------------------------------------------------
+// Wave64 collectives
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+// Number of set bits of `mask` in lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int t = __shfl_up(v, o, kWave);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+// Block-wide exclusive prefix sum of one int per thread (NT threads); also
+// returns the block total.  `sh` is LDS scratch of NT/64 + 1 ints.
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan(int v, int *sh, int &total) {
+    constexpr int NW = NT / kWave;
+    const int lane = lane_id(), wid = threadIdx.x / kWave;
+    int incl = wave_inclusive_scan(v);
+    if (lane == kWave - 1) sh[wid] = incl;
+    __syncthreads();
+    if (wid == 0) {
+        int wv = lane < NW ? sh[lane] : 0;
+        int wi = wave_inclusive_scan(wv);
+        if (lane < NW) sh[lane] = wi - wv;
+        if (lane == NW - 1) sh[NW] = wi;
+    }
+    __syncthreads();
+    int res = sh[wid] + incl - v;
+    total = sh[NW];
+    __syncthreads();
+    return res;
+}
+
+// ---------------------------------------------------------------------------
+// Block-wide k-th largest key (MSB-first radix search, 8-bit digits)
+// ---------------------------------------------------------------------------
+// Keys are held in registers: thread t owns indices t + r*NT, r < ITEMS.
+// Returns v = the k-th largest key (1 <= k <= n) and `need` = how many of the
+// keys equal to v belong to the top k (the rest of the top k is > v).
+// `hist` is LDS scratch of 256 + 2 uint32.
+template <int NT, int ITEMS, int KEYBITS>
+__device__ void block_kth_largest(const uint32_t (&keys)[ITEMS], int n, int k, uint32_t *hist,
+                                  uint32_t &v_out, int &need_out) {
+    const int tid = threadIdx.x;
+    uint32_t prefix = 0, pmask = 0;
+    int kk = k;
+#pragma unroll 1
+    for (int shift = ((KEYBITS - 1) / 8) * 8; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 256; b += NT) hist[b] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < ITEMS; ++r) {
+            const int i = tid + r * NT;
+            if (i < n && (keys[r] & pmask) == prefix)
+                atomicAdd(&hist[(keys[r] >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // Lane l owns bins 255-4l ... 252-4l (descending key order).
+            const int base = 255 - 4 * tid;
+            int c0 = hist[base], c1 = hist[base - 1], c2 = hist[base - 2], c3 = hist[base - 3];
+            int local = c0 + c1 + c2 + c3;
+            int incl = wave_inclusive_scan(local);
+            int excl = incl - local;
+            if (excl < kk && kk <= incl) {
+                int cum = excl, digit = base, q = 0;
+                const int c[4] = {c0, c1, c2, c3};
+                for (q = 0; q < 4; ++q) {
+                    if (cum + c[q] >= kk) break;
+                    cum += c[q];
+                }
+                digit = base - q;
+                hist[256] = (uint32_t)digit;
+                hist[257] = (uint32_t)cum;
+            }
+        }
+        __syncthreads();
+        const uint32_t digit = hist[256];
+        kk -= (int)hist[257];
+        prefix |= digit << shift;
+        pmask |= 255u << shift;
+        __syncthreads();
+    }
+    v_out = prefix;
+    need_out = kk;
+}
+
+}  // namespace prox

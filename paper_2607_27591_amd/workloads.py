@@ -18,15 +18,20 @@ row-major, i.e. ``gate_proj.weight``, ``up_proj.weight`` and
 directly in this layout is the same distribution as drawing the paper's
 ``W_gate in R^{d_model x d_ff}`` and transposing.
 
-Draw order per config (one ``numpy.random.default_rng(seed)`` stream, PCG64):
-``W_gate``, ``W_up``, ``W_down`` (each ``standard_normal(float32) * sigma``),
-then the outlier channel indices (``choice(d, n_out, replace=False)``), then
-the x vectors.  fp32 values are cast to bf16/fp16 with round-to-nearest-even.
+Random streams per config (numpy PCG64): weight matrix m (0 = W_gate,
+1 = W_up, 2 = W_down) is drawn in chunks of 2048 channel rows, chunk c from
+``default_rng([seed, m, c]).standard_normal(float32) * sigma`` (independent
+streams, so chunks are drawn in parallel); the outlier channel indices
+(``choice(d, n_out, replace=False)``) and then the x vectors come from
+``default_rng([seed, 3])``.  fp32 values are cast to bf16/fp16 with
+round-to-nearest-even.
 """
 from __future__ import annotations
 
 import dataclasses
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import List, Optional, Tuple
 
 import numpy as np
@@ -35,9 +40,9 @@ DT_F16 = 0
 DT_BF16 = 1
 DTYPE_NAMES = {DT_F16: "f16", DT_BF16: "bf16"}
 
-# Rows of weights drawn per numpy call; chunking bounds peak host memory and
-# produces the same stream as a single call (checked in the tests).
+# Channel rows of a weight matrix drawn from one child stream.
 _CHUNK_ROWS = 2048
+_THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
 def frac_to_k(frac: float, n: int) -> int:
@@ -114,11 +119,19 @@ def stack_layer_config(layer: int) -> FFNConfig:
 # Casting fp32 -> 16-bit patterns (round to nearest even)
 # ----------------------------------------------------------------------------
 
-def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+def f32_to_bf16_bits_ref(a: np.ndarray) -> np.ndarray:
     """fp32 -> bf16 bit patterns, round-to-nearest-even (finite inputs)."""
     u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
     r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even.  Uses torch's cast
+    (multi-threaded); the tests check it against f32_to_bf16_bits_ref."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
 def f32_to_f16_bits(a: np.ndarray) -> np.ndarray:
@@ -142,14 +155,21 @@ def bits_to_f32(bits: np.ndarray, dtype: int) -> np.ndarray:
 # Generators
 # ----------------------------------------------------------------------------
 
-def _draw_matrix(rng: np.random.Generator, rows: int, cols: int, sigma: float,
+def _draw_matrix(seed: int, m: int, rows: int, cols: int, sigma: float,
                  dtype: int) -> np.ndarray:
     out = np.empty((rows, cols), dtype=np.uint16)
-    for r0 in range(0, rows, _CHUNK_ROWS):
+
+    def chunk(c: int) -> None:
+        r0 = c * _CHUNK_ROWS
         r1 = min(rows, r0 + _CHUNK_ROWS)
-        blk = rng.standard_normal((r1 - r0, cols), dtype=np.float32)
+        blk = np.random.default_rng([seed, m, c]).standard_normal((r1 - r0, cols),
+                                                                 dtype=np.float32)
         blk *= np.float32(sigma)
         out[r0:r1] = to_bits(blk, dtype)
+
+    n = (rows + _CHUNK_ROWS - 1) // _CHUNK_ROWS
+    with ThreadPoolExecutor(_THREADS) as ex:
+        list(ex.map(chunk, range(n)))
     return out
 
 
@@ -183,14 +203,14 @@ def draw_x(rng: np.random.Generator, cfg: FFNConfig, n: int, batch: int,
 
 def make_workload(cfg: FFNConfig, weights: bool = True) -> Workload:
     """Weights and outlier channels for ``cfg`` in the documented draw order."""
-    rng = np.random.default_rng(cfg.seed)
     f, d = cfg.d_ff, cfg.d_model
     if weights:
-        wg = _draw_matrix(rng, f, d, cfg.sigma_w, cfg.dtype)
-        wu = _draw_matrix(rng, f, d, cfg.sigma_w, cfg.dtype)
-        wd = _draw_matrix(rng, f, d, cfg.sigma_w, cfg.dtype)
+        wg = _draw_matrix(cfg.seed, 0, f, d, cfg.sigma_w, cfg.dtype)
+        wu = _draw_matrix(cfg.seed, 1, f, d, cfg.sigma_w, cfg.dtype)
+        wd = _draw_matrix(cfg.seed, 2, f, d, cfg.sigma_w, cfg.dtype)
     else:
         wg = wu = wd = None
+    rng = np.random.default_rng([cfg.seed, 3])
     out = (rng.choice(d, cfg.n_outliers, replace=False).astype(np.int64)
            if cfg.n_outliers else np.zeros(0, np.int64))
     return Workload(cfg, wg, wu, wd, out, rng)

@@ -1,0 +1,142 @@
+"""Host-side checks of the C-ABI that need no GPU.
+
+The library must load, export every entry point include/prox.h declares, and
+reject bad arguments with the documented status codes before any HIP call
+(the pointers passed below are never dereferenced: validation fails first).
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_27591_amd import prox
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "prox.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = 0x100000          # 256-byte aligned, never dereferenced
+MISALIGNED = 0x100001
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(prox_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for must in ["prox_pack_proxy", "prox_ffn_dense", "prox_ffn_sparse", "prox_proxy_bytes",
+                 "prox_workspace_bytes", "prox_strerror"]:
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = prox.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", prox.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(prox_\w+)", out))
+    assert set(_declared()) <= exported
+
+
+def test_library_is_gfx950_only():
+    out = subprocess.run(["strings", prox.LIB_PATH], capture_output=True, text=True).stdout
+    assert "gfx950" in out
+    for other in ["gfx90a", "gfx942", "gfx1100", "sm_"]:
+        assert f"amdgcn-amd-amdhsa--{other}" not in out
+
+
+def _weights(d=1024, f=3072, dtype=prox.BF16, g=FAKE, u=FAKE, dn=FAKE):
+    return prox._Weights(d, f, dtype, g, u, dn)
+
+
+def _proxy(fmt=prox.INT4, group=128, blob=FAKE, nbytes=1 << 40):
+    return prox._Proxy(fmt, group, blob, nbytes)
+
+
+def _sparse(w=None, p=None, x=FAKE, B=1, k_in=10, k_ff=10, y=FAKE, mask=FAKE, ws=FAKE,
+            ws_bytes=1 << 40):
+    L = prox.lib()
+    w = w if w is not None else _weights()
+    p = p if p is not None else _proxy()
+    return L.prox_ffn_sparse(ctypes.byref(w), ctypes.byref(p), x, B, k_in, k_ff, y, mask, None,
+                             None, ws, ws_bytes, None)
+
+
+def test_sizes():
+    assert prox.proxy_bytes(8192, 28672, prox.INT4, 128) > 2 * 8192 * 28672 // 2
+    assert prox.proxy_bytes(1024, 3072, prox.INT8, 1024) > 2 * 1024 * 3072
+    assert prox.proxy_bytes(1000, 3072, prox.INT4, 128) == 0       # d % 128
+    assert prox.proxy_bytes(1024, 3072, prox.INT4, 96) == 0        # group % 128
+    assert prox.proxy_bytes(1024, 3072, prox.INT4, 512 * 3) == 0   # d % group
+    assert prox.proxy_bytes(1024, 3072, 7, 128) == 0               # fmt
+    assert prox.workspace_bytes(4096, 12288, 1) > 0
+    assert prox.workspace_bytes(4096, 12288, 17) == 0
+    assert prox.workspace_bytes(4096, 12288, 0) == 0
+    assert prox.workspace_bytes(32768, 12288, 1) == 0
+    assert prox.workspace_bytes(4096, 65537, 1) == 0
+    assert prox.workspace_bytes(4096, 12288, 16) > prox.workspace_bytes(4096, 12288, 1)
+
+
+def test_sparse_rejects_bad_arguments():
+    L = prox.lib()
+    assert _sparse(k_in=0) == INVALID
+    assert _sparse(k_in=1025) == INVALID
+    assert _sparse(k_ff=0) == INVALID
+    assert _sparse(k_ff=3073) == INVALID
+    assert _sparse(B=0) == INVALID
+    assert _sparse(B=17) == INVALID
+    assert _sparse(x=None) == INVALID
+    assert _sparse(y=None) == INVALID
+    assert _sparse(mask=None) == INVALID
+    assert _sparse(ws=None) == INVALID
+    assert _sparse(x=MISALIGNED) == INVALID
+    assert _sparse(ws=FAKE + 16) == INVALID
+    assert _sparse(w=_weights(g=0)) == INVALID
+    assert _sparse(w=_weights(dn=MISALIGNED)) == INVALID
+    assert _sparse(w=_weights(dtype=5)) == INVALID
+    assert _sparse(w=_weights(d=1000)) == UNSUPPORTED
+    assert _sparse(w=_weights(d=32768)) == UNSUPPORTED
+    assert _sparse(p=_proxy(group=96)) == UNSUPPORTED
+    assert _sparse(p=_proxy(fmt=9)) == UNSUPPORTED
+    assert _sparse(p=_proxy(nbytes=100)) == WORKSPACE
+    assert _sparse(ws_bytes=100) == WORKSPACE
+    p = _proxy()
+    w = _weights()
+    assert L.prox_ffn_sparse(ctypes.byref(w), None, FAKE, 1, 1, 1, FAKE, FAKE, None, None, FAKE,
+                             1 << 40, None) == INVALID
+    assert L.prox_ffn_sparse(None, ctypes.byref(p), FAKE, 1, 1, 1, FAKE, FAKE, None, None, FAKE,
+                             1 << 40, None) == INVALID
+    assert L.prox_ffn_sparse_staged(ctypes.byref(w), ctypes.byref(p), FAKE, 1, 1, 1, FAKE, FAKE,
+                                    None, None, FAKE, 1 << 40, None, None) == INVALID
+
+
+def test_dense_pack_norm_reject_bad_arguments():
+    L = prox.lib()
+    w = _weights()
+    assert L.prox_ffn_dense(ctypes.byref(w), FAKE, 0, FAKE, FAKE, 1 << 40, None) == INVALID
+    assert L.prox_ffn_dense(ctypes.byref(w), FAKE, 1, FAKE, FAKE, 10, None) == WORKSPACE
+    assert L.prox_ffn_dense(ctypes.byref(w), MISALIGNED, 1, FAKE, FAKE, 1 << 40, None) == INVALID
+    p = _proxy(nbytes=10)
+    assert L.prox_pack_proxy(ctypes.byref(w), ctypes.byref(p), None) == WORKSPACE
+    p = _proxy(group=1024 * 3)
+    assert L.prox_pack_proxy(ctypes.byref(w), ctypes.byref(p), None) == UNSUPPORTED
+    p = _proxy(blob=None)
+    assert L.prox_pack_proxy(ctypes.byref(w), ctypes.byref(p), None) == INVALID
+    p = _proxy()
+    assert L.prox_unpack_proxy(ctypes.byref(p), 1024, 3072, None, FAKE, FAKE, FAKE, None) == INVALID
+    assert L.prox_add_rmsnorm(FAKE, FAKE, 0, 1024, 1, ctypes.c_float(1e-6), FAKE, None) == INVALID
+    assert L.prox_add_rmsnorm(FAKE, FAKE, 1, 1024, 3, ctypes.c_float(1e-6), FAKE, None) == INVALID
+    assert L.prox_add_rmsnorm(FAKE, FAKE, 1, 1024, 1, ctypes.c_float(-1.0), FAKE, None) == INVALID
+
+
+def test_strerror_and_stage_names():
+    for s in range(5):
+        assert prox.strerror(s)
+    assert prox.stage_names() == ["select_inputs", "proxy_gemv_score", "select_channels",
+                                  "stage2_gate_up", "stage2_down"]
+    assert prox.lib().prox_sparse_stage_name(5) is None

@@ -1,0 +1,94 @@
+"""GPU parity at the full sizes of the synthetic workloads, in the launch
+configuration the benchmark times (the same prox_ffn_sparse call).  The CPU
+oracle is fast enough to evaluate every output at these sizes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_27591_amd import prox
+from paper_2607_27591_amd import workloads as W
+
+from gpu_cases import Y_TOL, check_pack, check_sparse, log, make_case, run_sparse, y_rel_err
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _full(name, n_vectors, dense=True):
+    cfg = W.CONFIGS[name]
+    log(f"[full] {name}: generating and packing")
+    case = make_case(cfg)
+    check_pack(case)
+    xs = case.wl.x_vectors(n_vectors, cfg.batch)
+    for n, x in enumerate(xs):
+        log(f"[full] {name} vector {n}")
+        out = run_sparse(case, x, cfg.k_in, cfg.k_ff)
+        log(f"    {check_sparse(case, x, cfg.k_in, cfg.k_ff, out, tag=f'{name}/{n}')}")
+    if dense:
+        log(f"[full] {name} dense")
+        y = prox.ffn_dense(case.w, prox.from_bits(xs[0], cfg.dtype))
+        torch.cuda.synchronize()
+        ref = oracle.ffn_dense(xs[0], cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down)
+        err = y_rel_err(prox.to_bits(y), ref, cfg.dtype)
+        log(f"    dense y err {err:.3e}")
+        assert err <= Y_TOL
+    del case
+    torch.cuda.empty_cache()
+
+
+def test_c1_1024x3072_f16_int8():
+    _full("c1_1024x3072_f16", 8)
+
+
+def test_c2_4096x12288_bf16():
+    _full("c2_4096x12288_bf16", 4)
+
+
+def test_c4_8192x28672_bf16():
+    _full("c4_8192x28672_bf16", 3)
+
+
+@pytest.fixture(scope="module")
+def c3_case():
+    cfg = W.CONFIGS["c3_4096x14336_bf16"]
+    log("[full] c3: generating and packing")
+    c = make_case(cfg)
+    yield c
+    del c
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("batch,sparsity", [(1, 0.0), (1, 0.5), (1, 0.7), (1, 0.9), (4, 0.7),
+                                            (4, 0.9), (16, 0.7), (16, 0.0)])
+def test_c3_batch_sparsity_sweep(c3_case, batch, sparsity):
+    cfg = c3_case.cfg
+    k_ff = W.frac_to_k(1.0 - sparsity, cfg.d_ff)
+    x = c3_case.wl.x_vectors(1, batch)[0]
+    log(f"[full] c3 B={batch} sparsity={sparsity} k_ff={k_ff}")
+    out = run_sparse(c3_case, x, cfg.k_in, k_ff)
+    log(f"    {check_sparse(c3_case, x, cfg.k_in, k_ff, out, tag=f'c3 B={batch} s={sparsity}')}")
+
+
+def test_c5_stack_teacher_forced():
+    """First layers of the 36-layer stack, each checked on the GPU's own input
+    x_l (masks may legitimately diverge over many layers), then the residual
+    RMSNorm x_{l+1} = RMSNorm(x_l + y_l) checked against the oracle."""
+    base = W.stack_layer_config(0)
+    x_bits = W.make_workload(base, weights=False).x_vectors(1, 1)[0]
+    x = prox.from_bits(x_bits, base.dtype)
+    for layer in range(3):
+        cfg = W.stack_layer_config(layer)
+        log(f"[full] c5 layer {layer}")
+        case = make_case(cfg)
+        xb = prox.to_bits(x)
+        out = run_sparse(case, xb, cfg.k_in, cfg.k_ff)
+        check_sparse(case, xb, cfg.k_in, cfg.k_ff, out, tag=f"c5 layer {layer}")
+        y = prox.from_bits(out.y, cfg.dtype)
+        x_next = prox.add_rmsnorm(x, y, 1e-6)
+        torch.cuda.synchronize()
+        ref = oracle.add_rmsnorm(xb, out.y, cfg.dtype, 1e-6)
+        got = W.bits_to_f32(prox.to_bits(x_next), cfg.dtype).astype(np.float64)
+        assert (np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6).all()
+        x = x_next
+        del case
+        torch.cuda.empty_cache()

@@ -5,13 +5,15 @@ import torch
 from paper_2607_27591_amd import workloads as W
 
 
-def test_chunked_draw_equals_single_draw(monkeypatch):
+def test_draw_recipe_is_reproducible(monkeypatch):
     cfg = W.small_config(d=64, f=300, seed=3)
     monkeypatch.setattr(W, "_CHUNK_ROWS", 7)
     a = W.make_workload(cfg)
-    rng = np.random.default_rng(cfg.seed)
-    wg = rng.standard_normal((cfg.d_ff, cfg.d_model), dtype=np.float32) * np.float32(cfg.sigma_w)
-    assert np.array_equal(a.w_gate, W.f32_to_bf16_bits(wg))
+    # chunk c of matrix m comes from default_rng([seed, m, c])
+    wu = np.concatenate([np.random.default_rng([cfg.seed, 1, c]).standard_normal(
+        (min(7, cfg.d_ff - 7 * c), cfg.d_model), dtype=np.float32) for c in range(43)])
+    wu *= np.float32(cfg.sigma_w)
+    assert np.array_equal(a.w_up, W.f32_to_bf16_bits_ref(wu))
     b = W.make_workload(cfg)
     assert np.array_equal(a.w_down, b.w_down)
     assert np.array_equal(a.x_vectors(3), b.x_vectors(3))
@@ -21,6 +23,7 @@ def test_bf16_and_f16_casts_are_rne():
     rng = np.random.default_rng(0)
     v = (rng.standard_normal(100000) * np.exp(rng.uniform(-10, 10, 100000))).astype(np.float32)
     want = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(W.f32_to_bf16_bits_ref(v), want)
     assert np.array_equal(W.f32_to_bf16_bits(v), want)
     want16 = torch.from_numpy(v).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(W.f32_to_f16_bits(v), want16)

@@ -1,0 +1,358 @@
+#!/usr/bin/env python3
+"""Benchmark of the Prox sparse SwiGLU FFN decode step on one MI355X.
+
+Default workload: the 8192 x 28672 bf16 FFN at batch 1 with an int4
+group-128 proxy, 40% of inputs and 30% of intermediate channels kept (70%
+FFN sparsity).  One step = one prox_ffn_sparse call (input top-k, proxy
+GEMV + score, channel top-k, gate/up, down) on a fresh decode vector, with
+weights, proxy and inputs already resident in HBM.
+
+Timing: every timed call is bracketed by HIP events on the stream the
+library launches on; before each call a 1 GiB buffer is rewritten (outside
+the events) so neither the L2s nor the 256 MB last-level cache hold weights
+("cold").  A back-to-back ("warm") figure is reported as secondary.  The
+dense HIP FFN is timed the same way.  Achieved bandwidth is computed from
+the bytes the sparse step has to move (algorithmic bytes), not from counters.
+
+Prints ONE JSON line.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sparse FFN µs/call + achieved HBM GB/s at 70% sparsity, batch 1 (vs dense)"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E peak
+ALPHA = 1.0 / 3.0              # proxy cost ratio used by the paper's cost model
+FLUSH_BYTES = 1 << 30
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c4_8192x28672_bf16",
+                    help="c1_1024x3072_f16 | c2_4096x12288_bf16 | c3_4096x14336_bf16 | "
+                         "c4_8192x28672_bf16 | c5_stack36")
+    ap.add_argument("--batch", type=int, default=None, help="batch rows (c3 sweeps 1/4/16)")
+    ap.add_argument("--ffn-sparsity", type=float, default=None,
+                    help="override the kept-channel fraction as 1 - sparsity")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--warm", action="store_true", help="headline from back-to-back calls")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(cfg, B, k_in, k_ff):
+    """Bytes the sparse step must move: x, the selected proxy rows, the
+    touched scale groups, the kept gate/up/down rows, and y."""
+    e, d, f = 2, cfg.d_model, cfg.d_ff
+    ng = d // cfg.group
+    return {
+        "x": B * d * e,
+        "proxy_codes": 2 * k_in * f * cfg.qbits // 8,
+        "proxy_scales": 2 * ng * f * 2,
+        "gate_up_rows": 2 * k_ff * d * e,
+        "down_rows": k_ff * d * e,
+        "y": B * d * e,
+    }
+
+
+def dense_bytes(cfg, B):
+    e, d, f = 2, cfg.d_model, cfg.d_ff
+    return 3 * d * f * e + 2 * B * d * e
+
+
+def src_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2607_27591_amd", "csrc", n), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel_src):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 PMC summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"pmc_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"traffic_json:\s*(\{.*\})", text)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_hash") != kernel_src:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def pct(v, q):
+    v = sorted(v)
+    return v[min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
+              "(the sparse decode step is single-GPU; sharding is described in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_27591_amd import prox
+    from paper_2607_27591_amd import workloads as W
+
+    prox.lib()   # fails loudly if libprox.so is missing
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+
+    if args.workload.startswith("c5"):
+        return bench_stack(args, np, torch, prox, W, dev)
+
+    cfg = W.CONFIGS[args.workload]
+    B = args.batch or cfg.batch
+    k_in = cfg.k_in
+    k_ff = cfg.k_ff if args.ffn_sparsity is None else W.frac_to_k(1 - args.ffn_sparsity, cfg.d_ff)
+    t_gen = time.perf_counter()
+    wl = W.make_workload(cfg)
+    n_x = min(args.warmup + args.steps, max(cfg.n_vectors, 1))
+    xs_np = wl.x_vectors(n_x, B)
+    w = prox.Weights(*(prox.from_bits(m, cfg.dtype, dev) for m in (wl.w_gate, wl.w_up, wl.w_down)))
+    proxy = prox.pack_proxy(w, prox.INT4 if cfg.qbits == 4 else prox.INT8, cfg.group)
+    xs = prox.from_bits(xs_np.reshape(n_x, B * cfg.d_model), cfg.dtype, dev).view(n_x, B, cfg.d_model)
+    ws = prox.new_workspace(cfg.d_model, cfg.d_ff, B, dev)
+    y = torch.empty((B, cfg.d_model), dtype=w.dtype, device=dev)
+    mask = torch.empty(cfg.d_ff, dtype=torch.uint8, device=dev)
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t_gen
+
+    def sparse(i, events=None):
+        prox.ffn_sparse(w, proxy, xs[i % n_x], k_in, k_ff, y=y, mask=mask, ws=ws, events=events)
+
+    def dense(i):
+        prox.ffn_dense(w, xs[i % n_x], y=y, ws=ws)
+
+    def timed(fn, n, cold=True, staged=False):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        stage = None
+        if staged:
+            stage = [[torch.cuda.Event(enable_timing=True) for _ in range(prox.SPARSE_STAGES + 1)]
+                     for _ in range(n)]
+            for row in stage:
+                for ev in row:
+                    ev.record()   # create the HIP events before handing them over
+        for i in range(n):
+            if cold:
+                flush.fill_(i & 0x7F)
+            evs[i][0].record()
+            if staged:
+                fn(i, stage[i])
+            else:
+                fn(i)
+            evs[i][1].record()
+        torch.cuda.synchronize()
+        us = [a.elapsed_time(b) * 1e3 for a, b in evs]
+        st = None
+        if staged:
+            st = [[row[s].elapsed_time(row[s + 1]) * 1e3 for s in range(prox.SPARSE_STAGES)]
+                  for row in stage]
+        return us, st
+
+    # ---- warmup ----
+    for i in range(args.warmup):
+        sparse(i)
+        if not args.no_dense:
+            dense(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K sparse steps ----
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    cold_us, _ = timed(sparse, args.steps, cold=not args.warm)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3
+
+    # Per-stage durations of the same kernels (staged entry point).
+    _, stage_rows = timed(sparse, args.steps, cold=not args.warm, staged=True)
+    stage_names = prox.stage_names()
+    stage_us = {n: statistics.mean(r[s] for r in stage_rows) for s, n in enumerate(stage_names)}
+
+    # Back-to-back calls between two events.
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        sparse(i)
+    e1.record()
+    torch.cuda.synchronize()
+    warm_us = e0.elapsed_time(e1) * 1e3 / args.steps
+
+    dense_us = None
+    if not args.no_dense:
+        dus, _ = timed(dense, args.steps, cold=not args.warm)
+        dense_us = statistics.median(dus)
+
+    ab = algorithmic_bytes(cfg, B, k_in, k_ff)
+    total_bytes = sum(ab.values())
+    med = statistics.median(cold_us)
+    mean = statistics.mean(cold_us)
+    gbs = total_bytes / (mean * 1e-6) / 1e9
+
+    # Dominant kernel: the fused Stage 2 kernel (three kept rows of d
+    # elements per kept channel, plus the f proxy scores it ranks).
+    s2_bytes = ab["gate_up_rows"] + ab["down_rows"] + 4 * cfg.d_ff
+    s2_us = stage_us["stage2_select_gate_up_down"]
+    s2_gbs = s2_bytes / (s2_us * 1e-6) / 1e9
+    traffic = measured_traffic(args.workload, src_hash("stage2.hip", "common.hpp", "layout.hpp",
+                                                       "topk.hpp"))
+    roofline = {"bound": "hbm", "kernel": "stage2_kernel (channel top-k, gate/up, down)",
+                "achieved": round(s2_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(s2_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": s2_bytes, "avg_launch_us": round(s2_us, 2)}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes)
+
+    s1 = 1 - k_in / cfg.d_model
+    s2 = 1 - k_ff / cfg.d_ff
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(mean / 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": W.DTYPE_NAMES[cfg.dtype],
+        "data": "synthetic: seeded i.i.d. Gaussian weights, heavy-tailed x (no checkpoint)",
+        "config": {"workload": f"{cfg.name}_b{B}", "d_model": cfg.d_model, "d_ff": cfg.d_ff,
+                   "batch": B, "k_in": k_in, "k_ff": k_ff,
+                   "proxy": f"int{cfg.qbits} group {cfg.group} fp16 scales",
+                   "ffn_sparsity_s2": round(s2, 4), "input_sparsity_s1": round(s1, 4),
+                   "paper_effective_sparsity_e": round(s2 - 2 * ALPHA * (1 - s1) / 3, 4)},
+        "us_per_call": {"mean": round(mean, 2), "median": round(med, 2),
+                        "p10": round(pct(cold_us, 0.1), 2), "p90": round(pct(cold_us, 0.9), 2),
+                        "warm_back_to_back": round(warm_us, 2),
+                        "protocol": "warm" if args.warm else "cold (1 GiB flush between calls)"},
+        "tokens_per_s": round(1e6 / mean, 1),
+        "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": total_bytes,
+        "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
+        "dense_us_per_call": None if dense_us is None else round(dense_us, 2),
+        "dense_gbs": None if dense_us is None else round(dense_bytes(cfg, B) / (dense_us * 1e-6) / 1e9, 1),
+        "speedup_vs_dense": None if dense_us is None else round(dense_us / med, 3),
+        "wall_ms_timed_region": round(wall_ms, 2),
+        "setup_s": round(gen_s, 2),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes):
+    """The CPU oracle as it stands, timed on this host on a bounded sample of
+    the same workload (proxy quantised once beforehand, untimed)."""
+    import oracle
+    cg, sg = oracle.quantize(wl.w_gate, cfg.dtype, cfg.qbits, cfg.group)
+    cu, su = oracle.quantize(wl.w_up, cfg.dtype, cfg.qbits, cfg.group)
+    n = 0
+    t0 = time.perf_counter()
+    while n < len(xs_np) and (time.perf_counter() - t0) < args.cpu_budget_s:
+        oracle.ffn_sparse(xs_np[n], cfg.dtype, wl.w_gate, wl.w_up, wl.w_down, k_in, k_ff,
+                          codes_g=cg, scales_g=sg, codes_u=cu, scales_u=su, group=cfg.group)
+        n += 1
+    dt = (time.perf_counter() - t0) / max(n, 1)
+    return {"value": round(total_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
+            "kind": "oracle", "us_per_call": round(dt * 1e6, 1),
+            "sample": f"{n} sparse decode calls of {cfg.name} at batch {B} "
+                      f"(fp64 C oracle, OpenMP; proxy quantised beforehand)"}
+
+
+def bench_stack(args, np, torch, prox, W, dev):
+    """36-layer stack: per token, prox_ffn_sparse then residual RMSNorm per
+    layer, back-to-back on one stream."""
+    L = W.STACK_LAYERS
+    layers = []
+    t_gen = time.perf_counter()
+    for l in range(L):
+        cfg = W.stack_layer_config(l)
+        wl = W.make_workload(cfg)
+        w = prox.Weights(*(prox.from_bits(m, cfg.dtype, dev) for m in (wl.w_gate, wl.w_up, wl.w_down)))
+        layers.append((w, prox.pack_proxy(w, prox.INT4, cfg.group)))
+        del wl
+    cfg = W.stack_layer_config(0)
+    x0 = prox.from_bits(W.make_workload(cfg, weights=False).x_vectors(1, 1)[0], cfg.dtype, dev)
+    ws = prox.new_workspace(cfg.d_model, cfg.d_ff, 1, dev)
+    y = torch.empty_like(x0)
+    x = torch.empty_like(x0)
+    mask = torch.empty(cfg.d_ff, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t_gen
+
+    def token(dense=False):
+        x.copy_(x0)
+        for w, p in layers:
+            if dense:
+                prox.ffn_dense(w, x, y=y, ws=ws)
+            else:
+                prox.ffn_sparse(w, p, x, cfg.k_in, cfg.k_ff, y=y, mask=mask, ws=ws)
+            prox.add_rmsnorm(x, y, 1e-6, out=x)
+
+    for _ in range(args.warmup):
+        token()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b in evs:
+        a.record(); token(); b.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3
+    us = [a.elapsed_time(b) * 1e3 for a, b in evs]
+    dense_us = None
+    if not args.no_dense:
+        token(dense=True)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.steps):
+            token(dense=True)
+        b.record()
+        torch.cuda.synchronize()
+        dense_us = a.elapsed_time(b) * 1e3 / args.steps
+    ab = sum(algorithmic_bytes(cfg, 1, cfg.k_in, cfg.k_ff).values()) * L
+    mean = statistics.mean(us)
+    gbs = ab / (mean * 1e-6) / 1e9
+    out = {"metric": "36-layer sparse FFN stack µs/token (back-to-back on one stream)",
+           "value": round(1e6 / mean, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(mean / 1e3, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "c5_stack36_4096x12288_bf16_b1", "layers": L,
+                      "k_in": cfg.k_in, "k_ff": cfg.k_ff},
+           "us_per_token": round(mean, 1), "achieved_gbs": round(gbs, 1),
+           "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "dense_us_per_token":
+               None if dense_us is None else round(dense_us, 1),
+           "speedup_vs_dense": None if dense_us is None else round(dense_us / mean, 3),
+           "protocol": "back-to-back tokens (12.7 GB of weights per token exceed the caches)",
+           "wall_ms_timed_region": round(wall_ms, 1), "setup_s": round(gen_s, 1)}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -49,7 +49,7 @@ typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1 } prox_qfmt;
 #define PROX_MIN_D_MODEL 128
 #define PROX_MAX_D_MODEL 16384   /* multiple of 128 */
 #define PROX_MAX_D_FF 65536
-#define PROX_SPARSE_STAGES 5     /* events recorded by prox_ffn_sparse_staged */
+#define PROX_SPARSE_STAGES 3     /* events recorded by prox_ffn_sparse_staged */
 
 /*
  * Original FFN weights (Sec. 2.1), all three channel-major: row j holds the
@@ -149,8 +149,9 @@ prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const vo
 /*
  * prox_ffn_sparse with timing: `events` holds PROX_SPARSE_STAGES + 1 caller-
  * created HIP events, recorded on `stream` before the first stage and after
- * each stage (input select, proxy GEMV + score, channel select, gate/up,
- * down + output).  Same kernels and launch configuration as prox_ffn_sparse.
+ * each stage: (0) input top-k + proxy GEMV + score, (1) channel top-k +
+ * gate/up + down partial sums, (2) reduction of the partial sums into y.
+ * Same kernels and launch configuration as prox_ffn_sparse.
  */
 prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, const void *x,
                                    int batch, int k_in, int k_ff, void *y, uint8_t *mask,

@@ -43,8 +43,7 @@ prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_E
 
 struct Ws {
     Ctrl *ctrl;
-    float *proxy_part, *scores, *s, *down_part;
-    int *ff_idx;
+    float *scores, *ypart;
 };
 
 Ws carve(void *ws, int d, int f, int batch) {
@@ -52,16 +51,34 @@ Ws carve(void *ws, int d, int f, int batch) {
     char *b = static_cast<char *>(ws);
     Ws w;
     w.ctrl = reinterpret_cast<Ctrl *>(b + L.ctrl);
-    w.proxy_part = reinterpret_cast<float *>(b + L.proxy_part);
     w.scores = reinterpret_cast<float *>(b + L.scores);
-    w.ff_idx = reinterpret_cast<int *>(b + L.ff_idx);
-    w.s = reinterpret_cast<float *>(b + L.s);
-    w.down_part = reinterpret_cast<float *>(b + L.down_part);
+    w.ypart = reinterpret_cast<float *>(b + L.ypart);
     return w;
 }
 
-const char *const kStageNames[PROX_SPARSE_STAGES] = {
-    "select_inputs", "proxy_gemv_score", "select_channels", "stage2_gate_up", "stage2_down"};
+const char *const kStageNames[PROX_SPARSE_STAGES] = {"proxy_gemv_score",
+                                                     "stage2_select_gate_up_down", "reduce_y"};
+
+// Stage 2 and the final reduction, shared by the sparse and the dense FFN
+// (scores == NULL: every channel).
+prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, int k_ff,
+                              const float *scores, uint8_t *mask, float *scores_copy, void *y,
+                              const Ws &W, hipEvent_t *events, hipStream_t stream) {
+    const int d = w->d_model, f = w->d_ff, dt = w->dtype;
+    const uint16_t *xb = static_cast<const uint16_t *>(x);
+    const int nwg = stage2_wgs(scores ? k_ff : f);
+    const int ystride = ypart_rows(batch);
+    for (int c0 = 0; c0 < batch; c0 += kStage2MaxNB) {
+        const int nb = batch - c0 < kStage2MaxNB ? batch - c0 : kStage2MaxNB;
+        PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, w->w_gate, w->w_up, w->w_down,
+                               scores, k_ff, W.ctrl, mask, c0 == 0 ? scores_copy : nullptr,
+                               W.ypart + (size_t)c0 * d, ystride, nwg, stream));
+    }
+    if (events) PROX_TRY(hipEventRecord(events[2], stream));
+    PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));
+    if (events) PROX_TRY(hipEventRecord(events[3], stream));
+    return PROX_OK;
+}
 
 prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
                         int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
@@ -86,32 +103,15 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
 
     const Ws W = carve(ws, d, f, batch);
     const int dt = w->dtype;
-    const uint16_t *xb = static_cast<const uint16_t *>(x);
-    auto rec = [&](int i) -> hipError_t {
-        return events ? hipEventRecord(events[i], stream) : hipSuccess;
-    };
-
-    PROX_TRY(rec(0));
-    PROX_TRY(launch_select_inputs(x, batch, d, k_in, W.ctrl, in_mask, stream));
-    PROX_TRY(rec(1));
-    for (int c0 = 0; c0 < batch; c0 += kProxyMaxNB) {
-        const int nb = batch - c0 < kProxyMaxNB ? batch - c0 : kProxyMaxNB;
-        PROX_TRY(launch_proxy(dt, qbits, xb + (size_t)c0 * d, nb, x, batch, d, f, p->group, p->blob,
-                              W.ctrl, W.proxy_part, W.scores, c0 > 0, stream));
+    if (events) PROX_TRY(hipEventRecord(events[0], stream));
+    const int pnb = proxy_max_nb(d);
+    for (int c0 = 0; c0 < batch; c0 += pnb) {
+        const int nb = batch - c0 < pnb ? batch - c0 : pnb;
+        PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob, W.ctrl,
+                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, stream));
     }
-    PROX_TRY(rec(2));
-    PROX_TRY(launch_select_channels(W.scores, f, k_ff, W.ctrl, mask, W.ff_idx, scores, stream));
-    PROX_TRY(rec(3));
-    for (int c0 = 0; c0 < batch; c0 += kGateUpMaxNB) {
-        const int nb = batch - c0 < kGateUpMaxNB ? batch - c0 : kGateUpMaxNB;
-        PROX_TRY(launch_gateup(dt, xb + (size_t)c0 * d, nb, d, w->w_gate, w->w_up, W.ff_idx, k_ff,
-                               W.s + (size_t)c0 * k_ff, k_ff, nullptr, stream));
-    }
-    PROX_TRY(rec(4));
-    PROX_TRY(launch_down(dt, w->w_down, d, W.ff_idx, k_ff, W.s, k_ff, batch, W.down_part, W.ctrl,
-                         y, stream));
-    PROX_TRY(rec(5));
-    return PROX_OK;
+    if (events) PROX_TRY(hipEventRecord(events[1], stream));
+    return stage2_and_reduce(w, x, batch, k_ff, W.scores, mask, scores, y, W, events, stream);
 }
 
 }  // namespace
@@ -180,15 +180,7 @@ prox_status prox_ffn_dense(const prox_weights *w, const void *x, int batch, void
     const int d = w->d_model, f = w->d_ff;
     if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
     const Ws W = carve(ws, d, f, batch);
-    const uint16_t *xb = static_cast<const uint16_t *>(x);
-    for (int c0 = 0; c0 < batch; c0 += kGateUpMaxNB) {
-        const int nb = batch - c0 < kGateUpMaxNB ? batch - c0 : kGateUpMaxNB;
-        PROX_TRY(launch_gateup(w->dtype, xb + (size_t)c0 * d, nb, d, w->w_gate, w->w_up, nullptr,
-                               f, W.s + (size_t)c0 * f, f, c0 == 0 ? W.ctrl : nullptr, stream));
-    }
-    PROX_TRY(launch_down(w->dtype, w->w_down, d, nullptr, f, W.s, f, batch, W.down_part, W.ctrl,
-                         y, stream));
-    return PROX_OK;
+    return stage2_and_reduce(w, x, batch, f, nullptr, nullptr, nullptr, y, W, nullptr, stream);
 }
 
 prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const void *x, int batch,

@@ -1,5 +1,5 @@
-// Host-side launchers of the libprox kernels (one per .hip file).  Each
-// enqueues on `s` and returns hipGetLastError().
+// Host-side launchers of the libprox kernels.  Each enqueues on `stream` and
+// returns the launch status.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -14,27 +14,24 @@ hipError_t launch_pack(int dtype, int qbits, const void *wg, const void *wu, int
 hipError_t launch_unpack(int qbits, const void *blob, int d, int f, int group, int8_t *cg,
                          uint16_t *sg, int8_t *cu, uint16_t *su, hipStream_t stream);
 
-hipError_t launch_select_inputs(const void *x, int B, int d, int k, Ctrl *ctrl, uint8_t *in_mask,
-                                hipStream_t stream);
-hipError_t launch_select_channels(const float *scores, int f, int k, Ctrl *ctrl, uint8_t *mask,
-                                  int *ff_idx, float *scores_copy, hipStream_t stream);
+// Stage 1 for batch rows [row0, row0 + nb) of x_all (nb <= proxy_max_nb(d));
+// the input top-k ranks all B_all rows.  accumulate != 0 keeps
+// max(previous, new) scores.
+int proxy_max_nb(int d);
+hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
+                        int d, int f, int group, int k_in, const void *blob, Ctrl *ctrl,
+                        uint8_t *in_mask, float *scores, int accumulate, hipStream_t stream);
 
-hipError_t launch_proxy(int dtype, int qbits, const void *x, int nb, const void *x_all, int B_all,
-                        int d, int f, int group, const void *blob, Ctrl *ctrl, float *part,
-                        float *scores, int accumulate, hipStream_t stream);
-
-hipError_t launch_gateup(int dtype, const void *x, int nb, int d, const void *wg, const void *wu,
-                         const int *ff_idx, int n_ch, float *s_out, int s_stride,
-                         Ctrl *ctrl_reset, hipStream_t stream);
-hipError_t launch_down(int dtype, const void *wd, int d, const int *ff_idx, int n_ch,
-                       const float *s, int s_stride, int nb, float *ypart, Ctrl *ctrl, void *y,
-                       hipStream_t stream);
+// Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
+// the dense FFN over all f channels.  Partial y rows go to
+// ypart[(w * ystride + b) * d + c] for workgroup w < nwg.
+hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
+                         const void *wu, const void *wd, const float *scores, int k_ff,
+                         Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                         int nwg, hipStream_t stream);
+hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
+                         hipStream_t stream);
 hipError_t launch_add_rmsnorm(int dtype, const void *x, const void *y, int batch, int d, float eps,
                               void *out, hipStream_t stream);
-
-// Geometry helpers shared with the host API (sizes, LDS limits).
-void down_geometry(int d, int n_ch, int &tiles, int &splits, int &ch_per_split);
-size_t down_lds_bytes(int nbt, int ch_per_split);
-int gateup_grid(int n_ch);
 
 }  // namespace prox

@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
         BlobHeader h{};
         h.magic = kBlobMagic; h.version = kBlobVersion; h.fmt = QB == 4 ? 1u : 0u;
         h.group = (uint32_t)group; h.d_model = (uint32_t)d; h.d_ff = (uint32_t)f;
-        h.tile = kTile; h.qbits = QB;
+        h.tile = (uint32_t)L.tile; h.qbits = QB;
         h.codes_offset = L.codes_offset; h.scales_offset = L.scales_offset;
         h.total_bytes = L.total;
         *reinterpret_cast<BlobHeader *>(blob) = h;
@@ -66,7 +66,8 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
     const int j0 = (rem % npairs) * 2;
     const uint16_t *w = mat == 0 ? wg : wu;
     constexpr int qmax = QB == 4 ? 7 : 127;
-    const int tile = j0 / kTile, c0 = j0 % kTile;
+    const int T = L.tile;
+    const int tile = j0 / T, c0 = j0 % T;
 
     double sigma[2];
     uint16_t sbits[2];
@@ -82,7 +83,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
         sigma[e] = f16_to_f64(sbits[e]);
     }
     uint16_t *scales = reinterpret_cast<uint16_t *>(blob + L.scales_offset);
-    const size_t sbase = (((size_t)tile * ng + g) * 2 + mat) * kTile + c0;
+    const size_t sbase = (((size_t)tile * ng + g) * 2 + mat) * T + c0;
     scales[sbase] = sbits[0];
     scales[sbase + 1] = sbits[1];
 
@@ -102,10 +103,10 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
         }
         uint8_t *seg = codes + ((size_t)tile * d + i) * L.row_bytes;
         if constexpr (QB == 4) {
-            seg[mat * (kTile / 2) + c0 / 2] = (uint8_t)((q[0] + 8) | ((q[1] + 8) << 4));
+            seg[mat * (T / 2) + c0 / 2] = (uint8_t)((q[0] + 8) | ((q[1] + 8) << 4));
         } else {
-            seg[mat * kTile + c0] = (uint8_t)(q[0] + 128);
-            seg[mat * kTile + c0 + 1] = (uint8_t)(q[1] + 128);
+            seg[mat * T + c0] = (uint8_t)(q[0] + 128);
+            seg[mat * T + c0 + 1] = (uint8_t)(q[1] + 128);
         }
     }
 }
@@ -122,19 +123,20 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint8_t *__restrict__
     const int mat = (int)(gid / ((long long)f * ng));
     const int rem = (int)(gid % ((long long)f * ng));
     const int j = rem / ng, g = rem % ng;
-    const int tile = j / kTile, c = j % kTile;
+    const int T = L.tile;
+    const int tile = j / T, c = j % T;
     const uint16_t *scales = reinterpret_cast<const uint16_t *>(blob + L.scales_offset);
-    (mat == 0 ? sg : su)[(size_t)j * ng + g] = scales[(((size_t)tile * ng + g) * 2 + mat) * kTile + c];
+    (mat == 0 ? sg : su)[(size_t)j * ng + g] = scales[(((size_t)tile * ng + g) * 2 + mat) * T + c];
     int8_t *out = (mat == 0 ? cg : cu) + (size_t)j * d;
     for (int ii = 0; ii < group; ++ii) {
         const int i = g * group + ii;
         const uint8_t *seg = blob + L.codes_offset + ((size_t)tile * d + i) * L.row_bytes;
         int q;
         if constexpr (QB == 4) {
-            const uint8_t byte = seg[mat * (kTile / 2) + c / 2];
+            const uint8_t byte = seg[mat * (T / 2) + c / 2];
             q = (int)((c & 1) ? (byte >> 4) : (byte & 15)) - 8;
         } else {
-            q = (int)seg[mat * kTile + c] - 128;
+            q = (int)seg[mat * T + c] - 128;
         }
         out[i] = (int8_t)q;
     }

@@ -1,64 +1,182 @@
-// Stage 2 exact sparse computation (Sec. 4.1 Stage 2) and the dense FFN
-// (Sec. 2.1), which runs the same kernels over every channel.
+// Stage 2 of the sparse decode step (Sec. 4.1 Stage 2) and the dense FFN
+// (Sec. 2.1), which runs the same kernel over every channel.
 //
-//  gate/up : for each kept channel j (one wave per channel), the contiguous
-//            rows W_gate[:, j] and W_up[:, j] are streamed with 16-byte loads
-//            and dotted with x (staged in LDS) by dot2 instructions in fp32;
-//            s_j = SiLU(g_j) u_j is kept in fp32.
-//  down    : y = sum_j s_j W_down[j, :] as a split-K GEMV.  A workgroup owns
-//            kDownCols output columns and one slice of the kept channels; its
-//            8 waves split the slice and are summed in LDS in wave order, the
-//            slices are summed by the last workgroup to arrive in slice order,
-//            and y is rounded once.  Deterministic: no floating-point atomics.
+// stage2_kernel, one workgroup per equal slice of the kept channels:
+//  prologue  (sparse only) every workgroup finds the channel threshold of the
+//            top-k_ff proxy scores itself, and the ascending global position
+//            of every kept channel, so it can take exactly its slice of the
+//            kept list (balanced to +-1 channel) without another launch.
+//  gate/up   the slice's channels are cut into (channel, part of d) units
+//            spread over the 16 waves; each unit streams two contiguous rows
+//            with 16-byte loads and dot2 instructions (fp32 accumulation);
+//            s_j = SiLU(g_j) u_j is kept in LDS in fp32.
+//  down      every thread owns 8 output columns and accumulates
+//            s_j W_down[j, c..c+8] over the slice; the workgroup writes one
+//            partial y.
+// reduce_kernel sums the partial y of all workgroups in workgroup order and
+// rounds y once.  No floating-point atomics: results are deterministic.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "topk.hpp"
 
 namespace prox {
 
-constexpr int kGuThreads = 512;
-constexpr int kDownThreads = kDownWaves * kWave;
+constexpr int kMaxSlice = (kMaxDFF + kStage2MaxWGs - 1) / kStage2MaxWGs;   // channels per WG
+constexpr int kMaxParts = 8;
 
-template <int NB, int DT>
-__global__ __launch_bounds__(kGuThreads) void gateup_kernel(
-    const uint16_t *__restrict__ x, int nb, int d, const uint16_t *__restrict__ wg,
-    const uint16_t *__restrict__ wu, const int *__restrict__ ff_idx, int n_ch,
-    float *__restrict__ s_out, int s_stride, Ctrl *__restrict__ ctrl_reset) {
-    extern __shared__ uint4 xs_vec[];   // [NB][d / 8] 16-byte vectors of x
-    const int nvec = d / 8;
-    for (int e = threadIdx.x; e < NB * nvec; e += kGuThreads) {
-        const int b = e / nvec, vv = e % nvec;
-        xs_vec[e] = b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv]
-                           : make_uint4(0, 0, 0, 0);
+// d is cut into Q parts for the gate/up units (each part >= 2048 columns).
+__host__ __device__ inline int gateup_parts(int d, int nbt) {
+    if (nbt > 2) return 1;
+    int q = d / 2048;
+    return q < 1 ? 1 : (q > kMaxParts ? kMaxParts : q);
+}
+
+__host__ __device__ inline bool x_in_lds(int d, int nbt) { return (size_t)nbt * d <= 32768; }
+
+// Thread groups sharing the down projection's channels (> 1 only when d/8 <
+// the block size), summed through LDS.
+__host__ __device__ inline int stage2_down_groups(int d, int nbt) {
+    const int ncg = d / 8;
+    return (ncg >= kBlock || nbt > 4) ? 1 : kBlock / ncg;
+}
+
+// Dynamic LDS ahead of s: x (when staged) or the down reduction buffer.
+__host__ __device__ inline size_t stage2_head_bytes(int d, int nbt) {
+    const size_t xbytes = x_in_lds(d, nbt) ? (size_t)nbt * d * 2 : 0;
+    const size_t red = stage2_down_groups(d, nbt) > 1 ? (size_t)(d / 8) * nbt * 8 * 4 : 0;
+    return xbytes > red ? xbytes : red;
+}
+
+// Score keys of one thread: the high halves in registers, the complete key
+// re-read from the scores (L2-resident) when the high half ties.
+template <int C2>
+struct ScoreKeys {
+    const uint32_t (&h2)[C2];
+    const float *scores;
+    int base;
+    __device__ uint32_t hi(int r) const {
+        const uint32_t w = h2[r >> 1];
+        return (r & 1) ? (w & 0xFFFF0000u) : (w << 16);
     }
-    if (ctrl_reset && blockIdx.x == 0)
-        for (int i = threadIdx.x; i < 256; i += kGuThreads) ctrl_reset->down_count[i] = 0;
+    __device__ uint32_t full(int r) const { return __float_as_uint(scores[base + r]); }
+};
+
+struct Stage2Smem {
+    int list[kMaxSlice];
+    float gu[kMaxSlice * kMaxParts * 2 * 2];   // [t][q][b][2] for nbt <= 2
+};
+
+template <int NB, int DT, int C>
+__global__ __launch_bounds__(kBlock) void stage2_kernel(
+    const uint16_t *__restrict__ x, int nb, int d, int f, const uint16_t *__restrict__ wg,
+    const uint16_t *__restrict__ wu, const uint16_t *__restrict__ wd,
+    const float *__restrict__ scores,   // NULL: dense FFN over all f channels
+    int k_ff, Ctrl *__restrict__ ctrl, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
+    float *__restrict__ ypart, int ypart_stride) {   // partial y rows per workgroup
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+    const int nwg = gridDim.x, w = blockIdx.x;
+    const bool sparse = scores != nullptr;
+    const int n_ch = sparse ? k_ff : f;
+    const int p0 = (int)((long long)w * n_ch / nwg), p1 = (int)((long long)(w + 1) * n_ch / nwg);
+    const int n = p1 - p0;   // channels of this workgroup
+
+    __shared__ TopKScratch tk;
+    __shared__ Stage2Smem sm;
+    extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
+
+    // ---- prologue: this workgroup's slice of the kept channels ----
+    if (sparse) {
+        // Thread t owns channels [t*c, t*c + c); only the high 16 bits of each
+        // score key stay in registers (two per VGPR).
+        const int c = (f + kBlock - 1) / kBlock;
+        const int base = tid * c;
+        uint32_t h2[C / 2];
+#pragma unroll
+        for (int q = 0; q < C / 2; ++q) {
+            // Scores are |s~| >= 0, so their IEEE bit patterns order like the values.
+            const int i0 = base + 2 * q;
+            const uint32_t a = (2 * q < c && i0 < f) ? __float_as_uint(scores[i0]) : 0u;
+            const uint32_t b = (2 * q + 1 < c && i0 + 1 < f) ? __float_as_uint(scores[i0 + 1]) : 0u;
+            h2[q] = (a >> 16) | (b & 0xFFFF0000u);
+        }
+        const ScoreKeys<C / 2> keys{h2, scores, base};
+        uint32_t v;
+        int need;
+        topk_threshold<kBlock, C>(keys, c, f, k_ff, tk, v, need);
+        int rank;
+        int pos = topk_positions<kBlock, C>(keys, c, f, v, need, tk, rank);
+        const int mchunk = (f + nwg - 1) / nwg;     // mask entries written by this workgroup
+        const int m_lo = w * mchunk, m_hi = m_lo + mchunk;
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            const int i = base + r;
+            if (r >= c || i >= f) continue;
+            const int cmp = topk_cmp(keys, r, v);
+            bool sel = cmp > 0;
+            if (cmp == 0) {
+                sel = rank < need;
+                if (w == 0 && rank == need - 1) {
+                    ctrl->ff_v = v;
+                    ctrl->ff_cut = (uint32_t)i;
+                }
+                ++rank;
+            }
+            if (sel) {
+                if (pos >= p0 && pos < p1) sm.list[pos - p0] = i;
+                ++pos;
+            }
+            if (i >= m_lo && i < m_hi) mask[i] = sel ? 1 : 0;
+            if (w == 0 && scores_copy) scores_copy[i] = scores[i];
+        }
+    } else {
+        for (int t = tid; t < n; t += kBlock) sm.list[t] = p0 + t;
+    }
+
+    const bool xl = x_in_lds(d, NB);
+    uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
+    const int nvec = d / 8;
+    if (xl) {
+        for (int e = tid; e < NB * nvec; e += kBlock) {
+            const int b = e / nvec, vv = e % nvec;
+            reinterpret_cast<uint4 *>(xs)[e] =
+                b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv] : make_uint4(0, 0, 0, 0);
+        }
+    }
     __syncthreads();
 
-    const int lane = lane_id();
-    const int waves = gridDim.x * (kGuThreads / kWave);
+    // ---- gate/up: units (channel t, part q) over the 16 waves ----
+    const int Q = gateup_parts(d, NB);
+    const int qv = nvec / Q;                                   // 16-byte vectors per part
+    float *s_sh = dyn + align_up(stage2_head_bytes(d, NB), 16) / 4;   // [slice][NB]
     constexpr int U = 4;
-    for (int t = blockIdx.x * (kGuThreads / kWave) + threadIdx.x / kWave; t < n_ch; t += waves) {
-        const int j = ff_idx ? ff_idx[t] : t;
+    for (int unit = wid; unit < n * Q; unit += kMaxBlockWaves) {
+        const int t = unit / Q, q = unit % Q;
+        const int j = sm.list[t];
         const uint4 *rg = reinterpret_cast<const uint4 *>(wg + (size_t)j * d);
         const uint4 *ru = reinterpret_cast<const uint4 *>(wu + (size_t)j * d);
+        const int v_begin = q * qv, v_end = (q == Q - 1) ? nvec : v_begin + qv;
         float ag[NB], au[NB];
 #pragma unroll
         for (int b = 0; b < NB; ++b) ag[b] = au[b] = 0.0f;
-        for (int v0 = lane; v0 < nvec; v0 += kWave * U) {
+        for (int v0 = v_begin + lane; v0 < v_end; v0 += kWave * U) {
             uint4 gv[U], uv[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                if (v0 + u * kWave < nvec) {
+                if (v0 + u * kWave < v_end) {
                     gv[u] = load_stream16(rg + v0 + u * kWave);
                     uv[u] = load_stream16(ru + v0 + u * kWave);
                 }
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                if (v0 + u * kWave < nvec) {
+                const int vv = v0 + u * kWave;
+                if (vv < v_end) {
 #pragma unroll
                     for (int b = 0; b < NB; ++b) {
-                        const uint4 xv = xs_vec[b * nvec + v0 + u * kWave];
+                        uint4 xv;
+                        if (xl) xv = reinterpret_cast<const uint4 *>(xs)[b * nvec + vv];
+                        else xv = b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv]
+                                         : make_uint4(0, 0, 0, 0);
                         ag[b] = dot2<DT>(xv.x, gv[u].x, ag[b]);
                         ag[b] = dot2<DT>(xv.y, gv[u].y, ag[b]);
                         ag[b] = dot2<DT>(xv.z, gv[u].z, ag[b]);
@@ -75,109 +193,143 @@ __global__ __launch_bounds__(kGuThreads) void gateup_kernel(
         for (int b = 0; b < NB; ++b) {
             const float gs = wave_sum(ag[b]);
             const float us = wave_sum(au[b]);
-            if (lane == 0 && b < nb) s_out[(size_t)b * s_stride + t] = silu(gs) * us;
+            if (lane == 0) {
+                if (Q == 1) {
+                    s_sh[t * NB + b] = silu(gs) * us;
+                } else {
+                    sm.gu[((t * Q + q) * 2 + b) * 2 + 0] = gs;
+                    sm.gu[((t * Q + q) * 2 + b) * 2 + 1] = us;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (Q > 1) {
+        for (int e = tid; e < n * NB; e += kBlock) {
+            const int t = e / NB, b = e % NB;
+            float gs = 0.0f, us = 0.0f;
+            for (int q = 0; q < Q; ++q) {
+                gs += sm.gu[((t * Q + q) * 2 + b) * 2 + 0];
+                us += sm.gu[((t * Q + q) * 2 + b) * 2 + 1];
+            }
+            s_sh[t * NB + b] = silu(gs) * us;
+        }
+        __syncthreads();
+    }
+
+    // ---- down: partial y over this slice ----
+    // d/8 groups of 8 columns; with fewer groups than threads (and NB <= 4)
+    // the channels are split over G thread groups, summed through LDS in
+    // group order.
+    const int ncg = d / 8;
+    const int G = stage2_down_groups(d, NB);
+    const int stride = G > 1 ? ncg : kBlock;
+    const int gi = tid / stride, cgt = tid % stride;
+    float *dred = dyn;   // reuses the x area: [ncg][NB][8]
+    constexpr int UD = 8;
+    for (int cg0 = 0; cg0 < ncg; cg0 += stride) {
+        const int cg = cg0 + cgt;
+        const bool active = cg < ncg && gi < G;
+        float acc[NB][8];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
+        if (active) {
+            for (int t0 = gi; t0 < n; t0 += G * UD) {
+                uint4 wv[UD];
+#pragma unroll
+                for (int u = 0; u < UD; ++u) {
+                    const int t = t0 + u * G;
+                    if (t < n) wv[u] = load_stream16(wd + (size_t)sm.list[t] * d + cg * 8);
+                }
+#pragma unroll
+                for (int u = 0; u < UD; ++u) {
+                    const int t = t0 + u * G;
+                    if (t < n) {
+                        const uint32_t w4[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
+                        float wf[8];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            wf[2 * q] = lo_to_float<DT>(w4[q]);
+                            wf[2 * q + 1] = hi_to_float<DT>(w4[q]);
+                        }
+#pragma unroll
+                        for (int b = 0; b < NB; ++b) {
+                            const float sv = s_sh[t * NB + b];
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
+                        }
+                    }
+                }
+            }
+        }
+        if (G > 1) {
+            // G > 1 implies ncg < kBlock, so this body runs exactly once and
+            // every thread reaches these barriers.
+            __syncthreads();   // x (aliased by dred) is no longer read
+            for (int g2 = 0; g2 < G; ++g2) {
+                if (active && gi == g2) {
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            float *dst = &dred[(cg * NB + b) * 8 + e];
+                            *dst = g2 == 0 ? acc[b][e] : *dst + acc[b][e];
+                        }
+                }
+                __syncthreads();
+            }
+            if (active && gi == 0) {
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[b][e] = dred[(cg * NB + b) * 8 + e];
+            }
+        }
+        if (active && gi == 0) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                if (b < nb) {
+                    float4 *dst = reinterpret_cast<float4 *>(ypart + ((size_t)w * ypart_stride + b) * d + cg * 8);
+                    dst[0] = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+                    dst[1] = make_float4(acc[b][4], acc[b][5], acc[b][6], acc[b][7]);
+                }
+            }
         }
     }
 }
 
-template <int NB, int DT>
-__global__ __launch_bounds__(kDownThreads) void down_kernel(
-    const uint16_t *__restrict__ wd, int d, const int *__restrict__ ff_idx, int n_ch,
-    const float *__restrict__ s, int s_stride, int nb, int ch_per_split,
-    float *__restrict__ ypart, Ctrl *__restrict__ ctrl, uint16_t *__restrict__ y) {
-    extern __shared__ float dsh[];   // idx[cps] | s[NB][cps] | red[NB][kDownCols]
-    int *idx_sh = reinterpret_cast<int *>(dsh);
-    float *s_sh = dsh + ch_per_split;
-    float *red_sh = s_sh + NB * ch_per_split;
-    __shared__ int last_sh;
-
-    const int tile = blockIdx.x, split = blockIdx.y, n_splits = gridDim.y;
-    const int t0 = split * ch_per_split;
-    const int n = max(0, min(n_ch - t0, ch_per_split));
-    for (int e = threadIdx.x; e < n; e += kDownThreads) {
-        idx_sh[e] = ff_idx ? ff_idx[t0 + e] : t0 + e;
-#pragma unroll
-        for (int b = 0; b < NB; ++b) s_sh[b * ch_per_split + e] = b < nb ? s[(size_t)b * s_stride + t0 + e] : 0.0f;
-    }
-    __syncthreads();
-
-    const int wid = threadIdx.x / kWave, lane = lane_id();
-    const int c0 = tile * kDownCols + lane * 8;
-    const bool active = c0 < d;
-    float acc[NB][8];
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
-    constexpr int U = 4;
-    if (active) {
-        for (int e0 = wid; e0 < n; e0 += kDownWaves * U) {
-            uint4 wv[U];
+// y[b][c] = sum over workgroups (in workgroup order) of the partial y, rounded
+// once.  A block covers 64 columns; its 16 waves take interleaved workgroups
+// and are summed in wave order.
+template <int DT>
+__global__ __launch_bounds__(kBlock) void reduce_kernel(const float *__restrict__ ypart, int nwg,
+                                                        int nbt, int d, uint16_t *__restrict__ y) {
+    __shared__ float red[kMaxBlockWaves][kWave];
+    const int b = blockIdx.y, wid = threadIdx.x / kWave, lane = lane_id();
+    const int c = blockIdx.x * kWave + lane;
+    float acc = 0.0f;
+    if (c < d) {
+        constexpr int U = 8;
+        for (int w0 = wid; w0 < nwg; w0 += kMaxBlockWaves * U) {
+            float v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kDownWaves;
-                if (e < n)
-                    wv[u] = load_stream16(wd + (size_t)idx_sh[e] * d + c0);
+                const int w = w0 + u * kMaxBlockWaves;
+                v[u] = w < nwg ? ypart[((size_t)w * nbt + b) * d + c] : 0.0f;
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kDownWaves;
-                if (e < n) {
-                    const uint32_t w4[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
-                    float wf[8];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        wf[2 * q] = lo_to_float<DT>(w4[q]);
-                        wf[2 * q + 1] = hi_to_float<DT>(w4[q]);
-                    }
-#pragma unroll
-                    for (int b = 0; b < NB; ++b) {
-                        const float sv = s_sh[b * ch_per_split + e];
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) acc[b][q] = fmaf(sv, wf[q], acc[b][q]);
-                    }
-                }
-            }
+            for (int u = 0; u < U; ++u) acc += v[u];
         }
     }
-    // Sum the 8 waves in wave order through one LDS tile.
-    for (int w = 0; w < kDownWaves; ++w) {
-        if (wid == w) {
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    float *dst = &red_sh[b * kDownCols + lane * 8 + q];
-                    *dst = w == 0 ? acc[b][q] : *dst + acc[b][q];
-                }
-        }
-        __syncthreads();
-    }
-    for (int e = threadIdx.x; e < nb * kDownCols; e += kDownThreads) {
-        const int b = e / kDownCols, c = e % kDownCols;
-        const int col = tile * kDownCols + c;
-        if (col < d) ypart[((size_t)split * NB + b) * d + col] = red_sh[b * kDownCols + c];
-    }
-
-    __threadfence();
+    red[wid][lane] = acc;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t prev = atomicAdd(&ctrl->down_count[tile], 1u);
-        last_sh = prev == (uint32_t)(n_splits - 1);
+    if (wid == 0 && c < d) {
+        float s = 0.0f;
+        for (int w = 0; w < kMaxBlockWaves; ++w) s += red[w][lane];
+        y[(size_t)b * d + c] = float_to_half<DT>(s);
     }
-    __syncthreads();
-    if (!last_sh) return;
-    __threadfence();
-    for (int e = threadIdx.x; e < nb * kDownCols; e += kDownThreads) {
-        const int b = e / kDownCols, c = e % kDownCols;
-        const int col = tile * kDownCols + c;
-        if (col >= d) continue;
-        float acc_y = 0.0f;
-        for (int sp = 0; sp < n_splits; ++sp)
-            acc_y += __builtin_nontemporal_load(&ypart[((size_t)sp * NB + b) * d + col]);
-        y[(size_t)b * d + col] = float_to_half<DT>(acc_y);
-    }
-    if (threadIdx.x == 0) ctrl->down_count[tile] = 0;
 }
 
 template <int DT>
@@ -198,7 +350,7 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(const uint16_t *__res
     float tot = 0.0f;
     for (int w = 0; w < 1024 / kWave; ++w) tot += wsum[w];
     const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-    __syncthreads();   // every thread has read x, y before out (which may alias x) is written
+    __syncthreads();   // every thread has read its x, y before out (which may alias x) is written
     for (int i = threadIdx.x; i < d; i += 1024) {
         const float r = half_to_float<DT>(xb[i]) + half_to_float<DT>(yb[i]);
         out[(size_t)b * d + i] = float_to_half<DT>(r * inv);
@@ -209,86 +361,72 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(const uint16_t *__res
 // Launchers
 // ---------------------------------------------------------------------------
 
-// Dynamic LDS above 64 KiB must be allowed per kernel (gfx950 has 160 KiB).
+size_t stage2_lds_bytes(int d, int nbt) {
+    return align_up(stage2_head_bytes(d, nbt), 16) + (size_t)kMaxSlice * nbt * 4;
+}
+
 template <typename K>
 static hipError_t allow_lds(K kernel, size_t bytes) {
+    // Dynamic LDS above 64 KiB must be allowed per kernel (gfx950 has 160 KiB).
     if (bytes <= 65536) return hipSuccess;
     return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-int gateup_grid(int n_ch) {
-    // Enough waves to cover the channels, at most 4 workgroups per CU.
-    const int waves_per_wg = kGuThreads / kWave;
-    int wgs = (n_ch + waves_per_wg - 1) / waves_per_wg;
-    return wgs < 1024 ? (wgs < 1 ? 1 : wgs) : 1024;
-}
-
-template <int NB, int DT>
-static void launch_gateup_t(const void *x, int nb, int d, const void *wg, const void *wu,
-                            const int *ff_idx, int n_ch, float *s_out, int s_stride,
-                            Ctrl *ctrl_reset, hipStream_t st) {
-    const size_t lds = (size_t)NB * d * sizeof(uint16_t);
-    if (allow_lds(gateup_kernel<NB, DT>, lds) != hipSuccess) return;
-    gateup_kernel<NB, DT><<<gateup_grid(n_ch), kGuThreads, lds, st>>>(
-        static_cast<const uint16_t *>(x), nb, d, static_cast<const uint16_t *>(wg),
-        static_cast<const uint16_t *>(wu), ff_idx, n_ch, s_out, s_stride, ctrl_reset);
-}
-
-hipError_t launch_gateup(int dtype, const void *x, int nb, int d, const void *wg, const void *wu,
-                         const int *ff_idx, int n_ch, float *s_out, int s_stride,
-                         Ctrl *ctrl_reset, hipStream_t st) {
-#define GU(NB_)                                                                                    \
-    (dtype == kBF16 ? launch_gateup_t<NB_, kBF16>(x, nb, d, wg, wu, ff_idx, n_ch, s_out, s_stride, \
-                                                   ctrl_reset, st)                                 \
-                    : launch_gateup_t<NB_, kF16>(x, nb, d, wg, wu, ff_idx, n_ch, s_out, s_stride,  \
-                                                  ctrl_reset, st))
-    if (nb == 1) GU(1);
-    else if (nb == 2) GU(2);
-    else GU(4);
-#undef GU
+template <int NB, int DT, int C>
+static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const void *wg,
+                                  const void *wu, const void *wd, const float *scores, int k_ff,
+                                  Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart,
+                                  int ystride, int nwg, hipStream_t st) {
+    const size_t lds = stage2_lds_bytes(d, NB);
+    hipError_t e = allow_lds(stage2_kernel<NB, DT, C>, lds);
+    if (e != hipSuccess) return e;
+    stage2_kernel<NB, DT, C><<<nwg, kBlock, lds, st>>>(
+        static_cast<const uint16_t *>(x), nb, d, f, static_cast<const uint16_t *>(wg),
+        static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff, ctrl,
+        mask, scores_copy, ypart, ystride);
     return hipGetLastError();
 }
 
-void down_geometry(int d, int n_ch, int &tiles, int &splits, int &ch_per_split) {
-    tiles = (d + kDownCols - 1) / kDownCols;
-    // About 16 channels per wave, at most kDownMaxSplits slices.
-    int sp = n_ch / (kDownWaves * 16);
-    sp = sp < 1 ? 1 : (sp > kDownMaxSplits ? kDownMaxSplits : sp);
-    ch_per_split = (n_ch + sp - 1) / sp;
-    splits = (n_ch + ch_per_split - 1) / ch_per_split;
-}
-
-size_t down_lds_bytes(int nbt, int ch_per_split) {
-    return (size_t)ch_per_split * sizeof(int) + (size_t)nbt * ch_per_split * sizeof(float) +
-           (size_t)nbt * kDownCols * sizeof(float);
-}
-
 template <int NB, int DT>
-static void launch_down_t(const void *wd, int d, const int *ff_idx, int n_ch, const float *s,
-                          int s_stride, int nb, float *ypart, Ctrl *ctrl, void *y, hipStream_t st) {
-    int tiles, splits, cps;
-    down_geometry(d, n_ch, tiles, splits, cps);
-    if (allow_lds(down_kernel<NB, DT>, down_lds_bytes(NB, cps)) != hipSuccess) return;
-    down_kernel<NB, DT><<<dim3(tiles, splits), kDownThreads, down_lds_bytes(NB, cps), st>>>(
-        static_cast<const uint16_t *>(wd), d, ff_idx, n_ch, s, s_stride, nb, cps, ypart, ctrl,
-        static_cast<uint16_t *>(y));
+static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const void *wg,
+                                  const void *wu, const void *wd, const float *scores, int k_ff,
+                                  Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart,
+                                  int ystride, int nwg, hipStream_t st) {
+    if (!scores || f <= 32 * kBlock)
+        return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,
+                                           scores_copy, ypart, ystride, nwg, st);
+    return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,
+                                       scores_copy, ypart, ystride, nwg, st);
 }
 
-hipError_t launch_down(int dtype, const void *wd, int d, const int *ff_idx, int n_ch,
-                       const float *s, int s_stride, int nb, float *ypart, Ctrl *ctrl, void *y,
-                       hipStream_t st) {
-#define DN(NB_)                                                                                 \
-    (dtype == kBF16 ? launch_down_t<NB_, kBF16>(wd, d, ff_idx, n_ch, s, s_stride, nb, ypart, ctrl, y, st) \
-                    : launch_down_t<NB_, kF16>(wd, d, ff_idx, n_ch, s, s_stride, nb, ypart, ctrl, y, st))
-    switch (down_nb_t(nb)) {
-        case 1: DN(1); break;
-        case 2: DN(2); break;
-        case 4: DN(4); break;
-        case 8: DN(8); break;
-        default: DN(16); break;
+hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
+                         const void *wu, const void *wd, const float *scores, int k_ff,
+                         Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                         int nwg, hipStream_t st) {
+#define S2(NB_)                                                                                    \
+    return dtype == kBF16                                                                          \
+               ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,    \
+                                             scores_copy, ypart, ystride, nwg, st)                 \
+               : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,     \
+                                            scores_copy, ypart, ystride, nwg, st)
+    switch (stage2_nb_t(nb)) {
+        case 1: S2(1);
+        case 2: S2(2);
+        case 4: S2(4);
+        default: S2(8);
     }
-#undef DN
+#undef S2
+}
+
+hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
+                         hipStream_t st) {
+    dim3 grid((d + kWave - 1) / kWave, nb);
+    const int nbt = ypart_rows(nb);
+    if (dtype == kBF16)
+        reduce_kernel<kBF16><<<grid, kBlock, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
+    else
+        reduce_kernel<kF16><<<grid, kBlock, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
     return hipGetLastError();
 }
 

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libprox.so")
 F16, BF16 = 0, 1
 INT8, INT4 = 0, 1
 MAX_BATCH = 16
-SPARSE_STAGES = 5
+SPARSE_STAGES = 3
 
 _TORCH_DT = {torch.float16: F16, torch.bfloat16: BF16}
 _DT_TORCH = {F16: torch.float16, BF16: torch.bfloat16}

@@ -137,6 +137,5 @@ def test_dense_pack_norm_reject_bad_arguments():
 def test_strerror_and_stage_names():
     for s in range(5):
         assert prox.strerror(s)
-    assert prox.stage_names() == ["select_inputs", "proxy_gemv_score", "select_channels",
-                                  "stage2_gate_up", "stage2_down"]
-    assert prox.lib().prox_sparse_stage_name(5) is None
+    assert prox.stage_names() == ["proxy_gemv_score", "stage2_select_gate_up_down", "reduce_y"]
+    assert prox.lib().prox_sparse_stage_name(3) is None

@@ -42,7 +42,6 @@ prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_E
     } while (0)
 
 struct Ws {
-    Ctrl *ctrl;
     float *scores, *ypart;
 };
 
@@ -50,7 +49,6 @@ Ws carve(void *ws, int d, int f, int batch) {
     const WsLayout L(d, f, batch);
     char *b = static_cast<char *>(ws);
     Ws w;
-    w.ctrl = reinterpret_cast<Ctrl *>(b + L.ctrl);
     w.scores = reinterpret_cast<float *>(b + L.scores);
     w.ypart = reinterpret_cast<float *>(b + L.ypart);
     return w;
@@ -71,7 +69,7 @@ prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, i
     for (int c0 = 0; c0 < batch; c0 += kStage2MaxNB) {
         const int nb = batch - c0 < kStage2MaxNB ? batch - c0 : kStage2MaxNB;
         PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, w->w_gate, w->w_up, w->w_down,
-                               scores, k_ff, W.ctrl, mask, c0 == 0 ? scores_copy : nullptr,
+                               scores, k_ff, mask, c0 == 0 ? scores_copy : nullptr,
                                W.ypart + (size_t)c0 * d, ystride, nwg, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
@@ -107,7 +105,7 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
     const int pnb = proxy_max_nb(d);
     for (int c0 = 0; c0 < batch; c0 += pnb) {
         const int nb = batch - c0 < pnb ? batch - c0 : pnb;
-        PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob, W.ctrl,
+        PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
                               c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[1], stream));

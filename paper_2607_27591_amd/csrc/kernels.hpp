@@ -19,7 +19,7 @@ hipError_t launch_unpack(int qbits, const void *blob, int d, int f, int group, i
 // max(previous, new) scores.
 int proxy_max_nb(int d);
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
-                        int d, int f, int group, int k_in, const void *blob, Ctrl *ctrl,
+                        int d, int f, int group, int k_in, const void *blob,
                         uint8_t *in_mask, float *scores, int accumulate, hipStream_t stream);
 
 // Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
@@ -27,7 +27,7 @@ hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int 
 // ypart[(w * ystride + b) * d + c] for workgroup w < nwg.
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
-                         Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                         uint8_t *mask, float *scores_copy, float *ypart, int ystride,
                          int nwg, hipStream_t stream);
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
                          hipStream_t stream);

@@ -21,20 +21,22 @@ __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a -
 // Proxy blob
 // ---------------------------------------------------------------------------
 // [0, 256)            header (BlobHeader)
-// codes               for each column tile t (T columns of d_ff; the last
-//                     tile zero-padded) and each input row i (0..d-1), one
+// codes               for each input row i (0..d-1) and each column tile t
+//                     (T columns of d_ff; the last tile zero-padded), one
 //                     contiguous segment: T gate codes then T up codes.
 //                     INT4: two codes per byte, even column in the low nibble,
 //                     stored as q + 8 (1..15).  INT8: one byte, q + 128.
-//                     Input-major, so the input-sparse proxy GEMV reads whole
-//                     segments of the kept rows.
+//                     Row-major over tiles: the segments of one kept input row
+//                     for all tiles are one contiguous run, and the workgroups
+//                     (one per tile) walk the same kept-row list in step, so
+//                     the input-sparse proxy GEMV reaches DRAM as long runs.
 // scales (256-aligned) for each tile t and group g: T gate scales then T up
 //                     scales, fp16 bits (0 in padded columns).
 // The tile width T is 128 when that already gives kProxyMinTiles column tiles
 // (one workgroup each), else 64.
 constexpr int kProxyMinTiles = 192;
 constexpr uint32_t kBlobMagic = 0x42585250u;  // "PRXB"
-constexpr uint32_t kBlobVersion = 2;
+constexpr uint32_t kBlobVersion = 3;
 
 __host__ __device__ inline int proxy_tile(int f) {
     return (f + 127) / 128 >= kProxyMinTiles ? 128 : 64;
@@ -47,7 +49,8 @@ struct BlobHeader {
 
 struct BlobLayout {
     int d, f, qbits, group, tile, n_tiles, f_pad;
-    size_t row_bytes;      // bytes of one (tile, row) segment: gate + up
+    size_t row_bytes;      // bytes of one (row, tile) segment: gate + up
+    size_t row_stride;     // bytes between the segments of rows i and i + 1
     size_t codes_offset, codes_bytes, scales_offset, scales_bytes, total;
     __host__ __device__ BlobLayout(int d_, int f_, int qbits_, int group_)
         : d(d_), f(f_), qbits(qbits_), group(group_) {
@@ -55,8 +58,9 @@ struct BlobLayout {
         n_tiles = (f + tile - 1) / tile;
         f_pad = n_tiles * tile;
         row_bytes = (size_t)2 * tile * qbits / 8;
+        row_stride = (size_t)n_tiles * row_bytes;
         codes_offset = 256;
-        codes_bytes = (size_t)n_tiles * d * row_bytes;
+        codes_bytes = (size_t)d * row_stride;
         scales_offset = align_up(codes_offset + codes_bytes, 256);
         scales_bytes = (size_t)n_tiles * (d / group) * 2 * tile * sizeof(uint16_t);
         total = align_up(scales_offset + scales_bytes, 256);
@@ -64,11 +68,8 @@ struct BlobLayout {
 };
 
 // ---------------------------------------------------------------------------
-// Stage 1: proxy GEMV + score, one workgroup per column tile.  Each of the 16
-// waves owns d / 16 consecutive input rows and walks them in windows of
-// kProxyWindow rows.
+// Stage 1: proxy GEMV + score, one workgroup per column tile.
 // ---------------------------------------------------------------------------
-constexpr int kProxyWindow = 256;
 constexpr int kProxyMaxNB = 4;           // batch rows per proxy launch
 
 __host__ __device__ inline int proxy_nb_t(int nb) { return nb <= 1 ? 1 : nb == 2 ? 2 : 4; }
@@ -101,17 +102,13 @@ __host__ __device__ inline int ypart_rows(int batch) {
 // ---------------------------------------------------------------------------
 // Workspace (no initialisation needed)
 // ---------------------------------------------------------------------------
-// ctrl (4 KiB): the two selection thresholds, for inspection.
-struct Ctrl {
-    uint32_t in_v, in_cut, ff_v, ff_cut;
-};
-
+// scores: the proxy scores (fp32, f padded to 128); ypart: per-workgroup
+// partial y rows of Stage 2.
 struct WsLayout {
-    size_t ctrl, scores, ypart, total;
+    size_t scores, ypart, total;
     __host__ __device__ WsLayout(int d, int f, int batch) {
         const int f_pad = (f + 127) / 128 * 128;
         size_t o = 0;
-        ctrl = o; o += 4096;
         scores = o; o = align_up(o + (size_t)f_pad * 4, 256);
         ypart = o; o = align_up(o + (size_t)kStage2MaxWGs * ypart_rows(batch) * d * 4, 256);
         total = o;

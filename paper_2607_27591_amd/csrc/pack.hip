@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
                 q[e] = (int)r;
             }
         }
-        uint8_t *seg = codes + ((size_t)tile * d + i) * L.row_bytes;
+        uint8_t *seg = codes + (size_t)i * L.row_stride + (size_t)tile * L.row_bytes;
         if constexpr (QB == 4) {
             seg[mat * (T / 2) + c0 / 2] = (uint8_t)((q[0] + 8) | ((q[1] + 8) << 4));
         } else {
@@ -130,7 +130,7 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint8_t *__restrict__
     int8_t *out = (mat == 0 ? cg : cu) + (size_t)j * d;
     for (int ii = 0; ii < group; ++ii) {
         const int i = g * group + ii;
-        const uint8_t *seg = blob + L.codes_offset + ((size_t)tile * d + i) * L.row_bytes;
+        const uint8_t *seg = blob + L.codes_offset + (size_t)i * L.row_stride + (size_t)tile * L.row_bytes;
         int q;
         if constexpr (QB == 4) {
             const uint8_t byte = seg[mat * (T / 2) + c / 2];

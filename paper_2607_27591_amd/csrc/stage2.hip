@@ -47,20 +47,9 @@ __host__ __device__ inline size_t stage2_head_bytes(int d, int nbt) {
     return xbytes > red ? xbytes : red;
 }
 
-// Score keys of one thread: the high halves in registers, the complete key
-// re-read from the scores (L2-resident) when the high half ties.
-template <int C2>
-struct ScoreKeys {
-    const uint32_t (&h2)[C2];
-    const float *scores;
-    int base;
-    __device__ uint32_t hi(int r) const {
-        const uint32_t w = h2[r >> 1];
-        return (r & 1) ? (w & 0xFFFF0000u) : (w << 16);
-    }
-    __device__ uint32_t full(int r) const { return __float_as_uint(scores[base + r]); }
-};
-
+// Score keys of one thread (item r = channel r * kBlock + base): the high
+// halves in registers, the complete key re-read from the scores
+// (L2-resident) when the high half ties.
 struct Stage2Smem {
     int list[kMaxSlice];
     float gu[kMaxSlice * kMaxParts * 2 * 2];   // [t][q][b][2] for nbt <= 2
@@ -71,7 +60,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const uint16_t *__restrict__ x, int nb, int d, int f, const uint16_t *__restrict__ wg,
     const uint16_t *__restrict__ wu, const uint16_t *__restrict__ wd,
     const float *__restrict__ scores,   // NULL: dense FFN over all f channels
-    int k_ff, Ctrl *__restrict__ ctrl, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
+    int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
     float *__restrict__ ypart, int ypart_stride) {   // partial y rows per workgroup
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
     const int nwg = gridDim.x, w = blockIdx.x;
@@ -81,53 +70,37 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const int n = p1 - p0;   // channels of this workgroup
 
     __shared__ TopKScratch tk;
+    __shared__ TopKOrder<C> ord;
     __shared__ Stage2Smem sm;
     extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
 
     // ---- prologue: this workgroup's slice of the kept channels ----
     if (sparse) {
-        // Thread t owns channels [t*c, t*c + c); only the high 16 bits of each
-        // score key stay in registers (two per VGPR).
-        const int c = (f + kBlock - 1) / kBlock;
-        const int base = tid * c;
-        uint32_t h2[C / 2];
+        // Item r of thread t is channel r * kBlock + t (coalesced loads).
+        // Scores are |s~| >= 0, so their IEEE bit patterns order like the
+        // values.  Clamped indices, masked later: all loads are in flight at once.
+        uint32_t key[C];
 #pragma unroll
-        for (int q = 0; q < C / 2; ++q) {
-            // Scores are |s~| >= 0, so their IEEE bit patterns order like the values.
-            const int i0 = base + 2 * q;
-            const uint32_t a = (2 * q < c && i0 < f) ? __float_as_uint(scores[i0]) : 0u;
-            const uint32_t b = (2 * q + 1 < c && i0 + 1 < f) ? __float_as_uint(scores[i0 + 1]) : 0u;
-            h2[q] = (a >> 16) | (b & 0xFFFF0000u);
+        for (int r = 0; r < C; ++r) {
+            key[r] = __float_as_uint(scores[min(r * kBlock + tid, f - 1)]);
         }
-        const ScoreKeys<C / 2> keys{h2, scores, base};
-        uint32_t v;
-        int need;
-        topk_threshold<kBlock, C>(keys, c, f, k_ff, tk, v, need);
-        int rank;
-        int pos = topk_positions<kBlock, C>(keys, c, f, v, need, tk, rank);
+        const uint64_t sel = topk_block<kBlock, C, true>(
+            key, f, k_ff, tk, ord, [scores](int i) { return __float_as_uint(scores[i]); });
         const int mchunk = (f + nwg - 1) / nwg;     // mask entries written by this workgroup
         const int m_lo = w * mchunk, m_hi = m_lo + mchunk;
 #pragma unroll
         for (int r = 0; r < C; ++r) {
-            const int i = base + r;
-            if (r >= c || i >= f) continue;
-            const int cmp = topk_cmp(keys, r, v);
-            bool sel = cmp > 0;
-            if (cmp == 0) {
-                sel = rank < need;
-                if (w == 0 && rank == need - 1) {
-                    ctrl->ff_v = v;
-                    ctrl->ff_cut = (uint32_t)i;
-                }
-                ++rank;
-            }
-            if (sel) {
+            const int i = r * kBlock + tid;
+            if (i >= f) continue;
+            const bool s = (sel >> r) & 1;
+            if (s) {
+                const int pos = topk_pos<C>(ord, r);
                 if (pos >= p0 && pos < p1) sm.list[pos - p0] = i;
-                ++pos;
             }
-            if (i >= m_lo && i < m_hi) mask[i] = sel ? 1 : 0;
-            if (w == 0 && scores_copy) scores_copy[i] = scores[i];
+            if (i >= m_lo && i < m_hi) mask[i] = s ? 1 : 0;
         }
+        if (scores_copy)
+            for (int i = m_lo + tid; i < min(m_hi, f); i += kBlock) scores_copy[i] = scores[i];
     } else {
         for (int t = tid; t < n; t += kBlock) sm.list[t] = p0 + t;
     }
@@ -376,14 +349,14 @@ static hipError_t allow_lds(K kernel, size_t bytes) {
 template <int NB, int DT, int C>
 static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
-                                  Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart,
+                                  uint8_t *mask, float *scores_copy, float *ypart,
                                   int ystride, int nwg, hipStream_t st) {
     const size_t lds = stage2_lds_bytes(d, NB);
     hipError_t e = allow_lds(stage2_kernel<NB, DT, C>, lds);
     if (e != hipSuccess) return e;
     stage2_kernel<NB, DT, C><<<nwg, kBlock, lds, st>>>(
         static_cast<const uint16_t *>(x), nb, d, f, static_cast<const uint16_t *>(wg),
-        static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff, ctrl,
+        static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff,
         mask, scores_copy, ypart, ystride);
     return hipGetLastError();
 }
@@ -391,24 +364,28 @@ static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const voi
 template <int NB, int DT>
 static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
-                                  Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart,
+                                  uint8_t *mask, float *scores_copy, float *ypart,
                                   int ystride, int nwg, hipStream_t st) {
-    if (!scores || f <= 32 * kBlock)
-        return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,
+    // C = score rows per thread of the channel top-k (the dense path has none).
+    if (!scores || f <= 16 * kBlock)
+        return launch_stage2_t<NB, DT, 16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
                                            scores_copy, ypart, ystride, nwg, st);
-    return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,
+    if (f <= 32 * kBlock)
+        return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
+                                           scores_copy, ypart, ystride, nwg, st);
+    return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
                                        scores_copy, ypart, ystride, nwg, st);
 }
 
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
-                         Ctrl *ctrl, uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                         uint8_t *mask, float *scores_copy, float *ypart, int ystride,
                          int nwg, hipStream_t st) {
 #define S2(NB_)                                                                                    \
     return dtype == kBF16                                                                          \
-               ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,    \
+               ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,    \
                                              scores_copy, ypart, ystride, nwg, st)                 \
-               : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, ctrl, mask,     \
+               : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,     \
                                             scores_copy, ypart, ystride, nwg, st)
     switch (stage2_nb_t(nb)) {
         case 1: S2(1);

@@ -1,23 +1,26 @@
 // Block-wide exact top-k, used in the prologues of the Stage 1 and Stage 2
 // kernels (App. A.6 per-token top-k rule, ties to the lower index).
 //
-// Thread t owns the contiguous items [t*c, t*c + c) of the n keys
-// (c = ceil(n / NT) <= C), so one block-wide prefix scan turns per-thread
-// counts into ascending global positions.  Keys are unsigned 32-bit; a key
-// accessor K provides them:
-//   K::hi(r)  the key of item r with its low 16 bits cleared (cheap, held in
-//             registers),
-//   K::full(r) the complete key (may read memory).
-// The full key is requested only for items whose high half equals the
-// threshold's, so callers can keep just 16 bits per key in registers.
+// Items are owned strided: item r of thread t is index r * NT + t, so every
+// key load is coalesced.  Keys are unsigned 32-bit and order like the values
+// they stand for (magnitude patterns, non-negative IEEE floats).
 //
-// The k-th largest key is found by an MSB-first radix search with 8-bit
-// digits, starting at the byte that holds the most significant bit of the
-// largest key.  Score and |x| keys are dominated by their exponent, so most
-// lanes of a wave fall in a handful of digits: the LDS histogram is
-// replicated kHistCopies times (lane l counts into copy l % kHistCopies, the
-// copies of one digit in adjacent banks), turning 64-way same-address atomics
-// into 4-way ones.
+// Fast path.  After a block max, every key is shifted left so that the
+// largest key's leading one sits at bit 31; the top 16 bits of the shifted
+// key (its "window") stay in registers, two per VGPR.  Two MSB-first radix
+// passes with 8-bit digits find the window value w* holding the k-th largest
+// key.  When all items with window w* are needed the selection is
+// {window >= w*}; otherwise, if at most one wave's worth of items share w*,
+// one wave ranks them by (full key descending, index ascending).  Any other
+// case (many equal windows) falls back to the general search below, which
+// resolves the full key and ties by index over ballots of the whole block.
+//
+// Each pass: atomics into an LDS histogram replicated kHistCopies times
+// (lane l counts into copy l % kHistCopies; score-like keys crowd a few
+// digits, and the copies turn 64-way same-address atomics into 4-way ones),
+// one barrier, all threads fold the copies (clearing them for the next pass),
+// one barrier, and every wave scans the 256 digit counts itself, so no
+// broadcast barrier is needed.
 #pragma once
 
 #include "common.hpp"
@@ -26,11 +29,23 @@ namespace prox {
 
 constexpr int kHistCopies = 16;
 
-struct TopKScratch {
-    uint32_t hist[256 * kHistCopies];   // [digit][copy]
+struct alignas(16) TopKScratch {
+    uint32_t hist[256 * kHistCopies];   // [digit][copy]; later selection words
+    uint32_t cnt[256];                  // folded digit counts
     uint32_t pick[2];
     uint32_t wmax[kMaxBlockWaves];
     int scan[kMaxBlockWaves + 1];
+    uint32_t cand_key[kWave];           // final-bucket candidates (fast path)
+    int cand_idx[kWave];
+    int cand_n;
+};
+
+// Per (item row r, wave w) ballots of the selected items and their exclusive
+// prefix counts in index order.
+template <int C>
+struct TopKOrder {
+    uint64_t sel[C][kMaxBlockWaves];
+    int off[C * kMaxBlockWaves];
 };
 
 template <int NT>
@@ -47,44 +62,59 @@ __device__ __forceinline__ uint32_t block_max_u32(uint32_t v, TopKScratch &sh) {
     return m;
 }
 
-// Key accessor over full 32-bit keys held in registers.
-template <int C>
-struct RegKeys {
-    const uint32_t (&k)[C];
-    __device__ uint32_t hi(int r) const { return k[r] & 0xFFFF0000u; }
-    __device__ uint32_t full(int r) const { return k[r]; }
-};
-
+// ---- general search (fallback) ----
+// Keys through an accessor K:
+//   K::hi(r)        the key of item r with its low 16 bits cleared, for a
+//                   compile-time r (held in registers),
+//   K::kHasLow      whether keys have low bits at all,
+//   K::full_dyn(r)  the complete key for a run-time r (reads memory).
+// Full keys are only read for items whose high half ties with the threshold
+// prefix, visited by a bit loop.
+//
 // v = the k-th largest of the n keys (1 <= k <= n); need = how many of the
 // keys equal to v belong to the top k (every key > v does).
 template <int NT, int C, typename K>
-__device__ void topk_threshold(const K &keys, int c, int n, int k, TopKScratch &sh,
-                               uint32_t &v_out, int &need_out) {
+__device__ __forceinline__ void topk_threshold(const K &keys, int n, int k, TopKScratch &sh, uint32_t &v_out,
+                               int &need_out) {
     const int tid = threadIdx.x, lane = lane_id();
     uint32_t kmax = 0;
 #pragma unroll
-    for (int r = 0; r < C; ++r)
-        if (r < c && tid * c + r < n) kmax = max(kmax, keys.hi(r));
+    for (int r = 0; r < C; ++r) {
+            if (r * NT + tid < n) kmax = max(kmax, keys.hi(r));
+    }
     kmax = block_max_u32<NT>(kmax, sh);
-    // With all high halves zero the search runs on the low half (full keys).
-    const int top_shift = kmax ? ((31 - __clz(kmax)) / 8) * 8 : 8;
+    // With every high half zero only the low half (if any) is searched.
+    const int top_shift = kmax ? ((31 - __clz(kmax)) / 8) * 8 : (K::kHasLow ? 8 : 16);
     uint32_t prefix = 0, pmask = 0;
     int kk = k;
     const int copy = lane % kHistCopies;
+    uint64_t cand = 0;   // items whose high half matches the prefix (low-half passes)
+    const int last_shift = K::kHasLow ? 0 : 16;
 #pragma unroll 1
-    for (int shift = top_shift; shift >= 0; shift -= 8) {
+    for (int shift = top_shift; shift >= last_shift; shift -= 8) {
         for (int b = tid; b < 256 * kHistCopies / 4; b += NT)
             reinterpret_cast<uint4 *>(sh.hist)[b] = make_uint4(0, 0, 0, 0);
         __syncthreads();
-        const uint32_t hmask = pmask & 0xFFFF0000u, hpref = prefix & 0xFFFF0000u;
+        if (shift >= 16) {
 #pragma unroll
-        for (int r = 0; r < C; ++r) {
-            if (r >= c || tid * c + r >= n) continue;
-            const uint32_t kh = keys.hi(r);
-            if ((kh & hmask) != hpref) continue;
-            const uint32_t key = shift >= 16 ? kh : keys.full(r);
-            if ((key & pmask) == prefix)
-                atomicAdd(&sh.hist[((key >> shift) & 255u) * kHistCopies + copy], 1u);
+            for (int r = 0; r < C; ++r) {
+                if (r * NT + tid >= n) continue;
+                const uint32_t kh = keys.hi(r);
+                if ((kh & pmask) == prefix)
+                    atomicAdd(&sh.hist[((kh >> shift) & 255u) * kHistCopies + copy], 1u);
+            }
+        } else {
+            if (shift == 8) {   // the high half is settled: collect its ties once
+#pragma unroll
+                for (int r = 0; r < C; ++r) {
+                        if (r * NT + tid < n && keys.hi(r) == (prefix & 0xFFFF0000u)) cand |= 1ull << r;
+                }
+            }
+            for (uint64_t m = cand; m; m &= m - 1) {
+                const uint32_t key = keys.full_dyn(__builtin_ctzll(m));
+                if ((key & pmask) == prefix)
+                    atomicAdd(&sh.hist[((key >> shift) & 255u) * kHistCopies + copy], 1u);
+            }
         }
         __syncthreads();
         if (tid < kWave) {
@@ -126,36 +156,261 @@ __device__ void topk_threshold(const K &keys, int c, int n, int k, TopKScratch &
     need_out = kk;
 }
 
-// Compare item r with the threshold v: +1 if key > v, 0 if equal, -1 if less.
-template <typename K>
-__device__ __forceinline__ int topk_cmp(const K &keys, int r, uint32_t v) {
-    const uint32_t kh = keys.hi(r), vh = v & 0xFFFF0000u;
-    if (kh != vh) return kh > vh ? 1 : -1;
-    const uint32_t kf = keys.full(r);
-    return kf > v ? 1 : (kf == v ? 0 : -1);
+// Exclusive scan, in (r, w) order, of the C * 16 per-wave counts in off[]
+// (written before the call by lane 0 of each wave).  One wave does it: lane l
+// holds C / 4 consecutive entries.
+template <int NT, int C>
+__device__ __forceinline__ void topk_scan_table(int *off, TopKScratch &) {
+    static_assert(C % 4 == 0 && C * kMaxBlockWaves == kWave * (C / 4), "C / 4 entries per lane");
+    constexpr int E = C / 4;
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        const int lane = lane_id();
+        int v[E], run = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            v[e] = run;
+            run += off[lane * E + e];
+        }
+        const int base = wave_inclusive_scan(run) - run;
+#pragma unroll
+        for (int e = 0; e < E; ++e) off[lane * E + e] = base + v[e];
+    }
+    __syncthreads();
 }
 
-// Given the threshold (v, need), returns the ascending global position of
-// this thread's first selected key and sets `eq_rank0` to the number of keys
-// equal to v in earlier threads.  Item r is selected iff key > v, or key == v
-// and its rank among the keys equal to v is < need.
+// Selection bits of the top k given v and need from topk_threshold (bit r =
+// item r); ord.off serves as scratch for ranking the keys equal to v.
 template <int NT, int C, typename K>
-__device__ int topk_positions(const K &keys, int c, int n, uint32_t v, int need, TopKScratch &sh,
-                              int &eq_rank0) {
-    const int tid = threadIdx.x;
-    int n_gt = 0, n_eq = 0;
+__device__ __forceinline__ uint64_t topk_select_general(const K &keys, int n, uint32_t v, int need,
+                                                        TopKScratch &sh, TopKOrder<C> &ord) {
+    static_assert(C <= 64, "selection bits fit in 64");
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+    uint64_t gt = 0, eq = 0;
+    const uint32_t vh = v & 0xFFFF0000u;
 #pragma unroll
     for (int r = 0; r < C; ++r) {
-        if (r < c && tid * c + r < n) {
-            const int cmp = topk_cmp(keys, r, v);
-            n_gt += cmp > 0;
-            n_eq += cmp == 0;
+        if (r * NT + tid >= n) continue;
+        const uint32_t kh = keys.hi(r);
+        gt |= (uint64_t)(kh > vh) << r;
+        eq |= (uint64_t)(kh == vh) << r;
+    }
+    if (K::kHasLow) {   // settle high-half ties on the full key
+        for (uint64_t m = eq; m; m &= m - 1) {
+            const int r = __builtin_ctzll(m);
+            const uint32_t kf = keys.full_dyn(r);
+            if (kf > v) gt |= 1ull << r;
+            if (kf != v) eq &= ~(1ull << r);
         }
     }
-    int total;
-    eq_rank0 = block_exclusive_scan<NT>(n_eq, sh.scan, total);
-    const int my_eq = max(0, min(need - eq_rank0, n_eq));
-    return block_exclusive_scan<NT>(n_gt + my_eq, sh.scan, total);
+    // Rank the keys equal to v in index order; the first `need` are kept.
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        const uint64_t m = __ballot((eq >> r) & 1);
+        if (lane == 0) ord.off[r * kMaxBlockWaves + wid] = __popcll(m);
+    }
+    topk_scan_table<NT, C>(ord.off, sh);
+    uint64_t sel = gt;
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        const uint64_t m = __ballot((eq >> r) & 1);
+        if ((eq >> r) & 1) {
+            const int rank = ord.off[r * kMaxBlockWaves + wid] + (int)lanes_below(m);
+            if (rank < need) sel |= 1ull << r;
+        }
+    }
+    __syncthreads();   // ord.off is rewritten by topk_order
+    return sel;
+}
+
+// Ascending positions of the selected items: per (row, wave) ballots and their
+// exclusive prefix counts in index order.
+template <int NT, int C>
+__device__ __forceinline__ void topk_order(uint64_t sel, int n, TopKScratch &sh, TopKOrder<C> &ord) {
+    static_assert(C <= kWave, "one row per lane");
+    const int wid = threadIdx.x / kWave, lane = lane_id();
+    uint64_t mine = 0;   // lane r keeps row r's ballot (rows past n stay empty)
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        const uint64_t m = __ballot((sel >> r) & 1);
+        mine = lane == r ? m : mine;
+    }
+    if (lane < C) {
+        ord.sel[lane][wid] = mine;
+        ord.off[lane * kMaxBlockWaves + wid] = __popcll(mine);
+    }
+    topk_scan_table<NT, C>(ord.off, sh);
+}
+
+// ---- fast path ----
+// One radix pass over the items for which item(r, digit) is true: returns the
+// digit holding the kk-th largest (counting from the top), kk's rank inside
+// that digit, and the digit's item count.  sh.hist must be zero on entry and
+// is zero again on return.
+template <int NT, int C, typename Item>
+__device__ __forceinline__ void topk_pass(const Item &item, int n, TopKScratch &sh, int &kk,
+                                          uint32_t &digit, int &bucket) {
+    static_assert(NT == 256 * kHistCopies / 4, "one uint4 of copies per thread");
+    const int tid = threadIdx.x, lane = lane_id();
+    const int copy = lane % kHistCopies;
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        uint32_t dg;
+        if (item(r, dg)) atomicAdd(&sh.hist[dg * kHistCopies + copy], 1u);
+    }
+    __syncthreads();
+    {
+        const int dgt = tid / 4;
+        uint4 *h = reinterpret_cast<uint4 *>(&sh.hist[dgt * kHistCopies]) + (tid % 4);
+        const uint4 c4 = *h;
+        *h = make_uint4(0, 0, 0, 0);
+        uint32_t t = c4.x + c4.y + c4.z + c4.w;
+        t += (uint32_t)__shfl_xor((int)t, 1, kWave);
+        t += (uint32_t)__shfl_xor((int)t, 2, kWave);
+        if ((tid % 4) == 0) sh.cnt[dgt] = t;
+    }
+    __syncthreads();
+    // Lane l holds digits 255-4l ... 252-4l (descending key order).
+    const uint4 c4 = *reinterpret_cast<const uint4 *>(&sh.cnt[252 - 4 * lane]);
+    const int c0 = (int)c4.w, c1 = (int)c4.z, c2 = (int)c4.y, c3 = (int)c4.x;
+    const int local = c0 + c1 + c2 + c3;
+    const int incl = wave_inclusive_scan(local);
+    const int excl = incl - local;
+    const uint64_t hit = __ballot(excl < kk && kk <= incl);
+    const int src = __builtin_ctzll(hit);   // exactly one lane: 1 <= kk <= total
+    int q, cum = excl, cq;
+    if (kk <= cum + c0) { q = 0; cq = c0; }
+    else if (kk <= cum + c0 + c1) { q = 1; cum += c0; cq = c1; }
+    else if (kk <= cum + c0 + c1 + c2) { q = 2; cum += c0 + c1; cq = c2; }
+    else { q = 3; cum += c0 + c1 + c2; cq = c3; }
+    digit = (uint32_t)__shfl(255 - 4 * lane - q, src, kWave);
+    kk -= __shfl(cum, src, kWave);
+    bucket = __shfl(cq, src, kWave);
+}
+
+// Window keys (top 16 bits of the shifted keys) for the general search.
+template <int NT, int C2, bool HL, typename Reload>
+struct WinKeys {
+    static constexpr bool kHasLow = HL;
+    const uint32_t (&h2)[C2];
+    const Reload &reload;
+    int shift;
+    __device__ uint32_t hi(int r) const {
+        const uint32_t w = h2[r >> 1];
+        return (r & 1) ? (w & 0xFFFF0000u) : (w << 16);
+    }
+    __device__ uint32_t full_dyn(int r) const { return reload(r * NT + (int)threadIdx.x) << shift; }
+};
+
+// Top k of n keys (1 <= k <= n).  key[r] is item r's key (any value when its
+// index is >= n); reload(i) returns key i again (only called when kHasLow:
+// keys with bits below their 16-bit window).  Returns the selection bits and
+// fills ord with the ascending positions of the selected items.
+template <int NT, int C, bool kHasLow, typename Reload>
+__device__ __forceinline__ uint64_t topk_block(const uint32_t (&key)[C], int n, int k, TopKScratch &sh,
+                                               TopKOrder<C> &ord, const Reload &reload) {
+    static_assert(C % 2 == 0 && C <= 64, "paired windows, 64 selection bits");
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+    // Block max (valid items), with the histogram cleared behind it.
+    uint32_t kmax = 0;
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+            if (r * NT + tid < n) kmax = max(kmax, key[r]);
+    }
+    for (int b = tid; b < 256 * kHistCopies / 4; b += NT)
+        reinterpret_cast<uint4 *>(sh.hist)[b] = make_uint4(0, 0, 0, 0);
+    kmax = block_max_u32<NT>(kmax, sh);
+    const int shift = kmax ? __clz(kmax) : 0;
+    uint32_t h2[C / 2];
+#pragma unroll
+    for (int q = 0; q < C / 2; ++q)   // rows past n hold junk and are never read
+        h2[q] = ((key[2 * q] << shift) >> 16) | ((key[2 * q + 1] << shift) & 0xFFFF0000u);
+    auto win = [&](int r) -> uint32_t { return (r & 1) ? (h2[r >> 1] >> 16) : (h2[r >> 1] & 0xFFFFu); };
+    auto valid = [&](int r) { return r * NT + tid < n; };
+
+    int kk = k, bucket;
+    uint32_t da, db;
+    topk_pass<NT, C>([&](int r, uint32_t &dg) { dg = win(r) >> 8; return valid(r); }, n, sh, kk, da, bucket);
+    uint64_t sel = 0;
+    if (kk == bucket) {   // every item with this top digit is in
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            sel |= (uint64_t)(valid(r) && (win(r) >> 8) >= da) << r;
+        }
+    } else {
+        if (tid == 0) sh.cand_n = 0;   // not touched again before the next barrier
+        topk_pass<NT, C>([&](int r, uint32_t &dg) { dg = win(r) & 255u; return valid(r) && (win(r) >> 8) == da; },
+                         n, sh, kk, db, bucket);
+        const uint32_t w_star = (da << 8) | db;
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            sel |= (uint64_t)(valid(r) && win(r) > w_star) << r;
+        }
+        if (kk == bucket) {
+#pragma unroll
+            for (int r = 0; r < C; ++r) {
+                sel |= (uint64_t)(valid(r) && win(r) == w_star) << r;
+            }
+        } else if (bucket <= kWave) {
+            // Gather the bucket (slot order is arbitrary; ranking is explicit).
+            // The histogram is idle now: its first NT 64-bit words become
+            // per-thread selection words for the bucket items.
+            uint64_t *selw = reinterpret_cast<uint64_t *>(sh.hist);
+            static_assert(sizeof(sh.hist) >= NT * sizeof(uint64_t), "selection words fit");
+            selw[tid] = 0;
+#pragma unroll
+            for (int r = 0; r < C; ++r) {
+                if (valid(r) && win(r) == w_star) {
+                    const int i = r * NT + tid;
+                    const int slot = atomicAdd(&sh.cand_n, 1);
+                    sh.cand_key[slot] = kHasLow ? reload(i) << shift : w_star << 16;
+                    sh.cand_idx[slot] = i;
+                }
+            }
+            __syncthreads();
+            if (wid == 0 && lane < bucket) {
+                const uint32_t mk = sh.cand_key[lane];
+                const int mi = sh.cand_idx[lane];
+                int rank = 0;
+                for (int j = 0; j < bucket; ++j) {
+                    const uint32_t kj = sh.cand_key[j];
+                    const int ij = sh.cand_idx[j];
+                    rank += (kj > mk || (kj == mk && ij < mi)) ? 1 : 0;
+                }
+                if (rank < kk) atomicOr(reinterpret_cast<unsigned long long *>(&selw[mi % NT]), 1ull << (mi / NT));
+            }
+            __syncthreads();
+            sel |= selw[tid];
+        } else {
+            // Many items share the window: general search on the shifted keys.
+            const WinKeys<NT, C / 2, kHasLow, Reload> wk{h2, reload, shift};
+            uint32_t v;
+            int need;
+            topk_threshold<NT, C>(wk, n, k, sh, v, need);
+            sel = topk_select_general<NT, C>(wk, n, v, need, sh, ord);
+        }
+    }
+    topk_order<NT, C>(sel, n, sh, ord);
+    return sel;
+}
+
+// Ascending position (among the selected) of this thread's selected item r.
+template <int C>
+__device__ __forceinline__ int topk_pos(const TopKOrder<C> &ord, int r) {
+    const int wid = threadIdx.x / kWave;
+    return ord.off[r * kMaxBlockWaves + wid] + (int)lanes_below(ord.sel[r][wid]);
+}
+
+// Number of selected items with index < i (0 <= i <= C * NT), any thread.
+template <int NT, int C>
+__device__ __forceinline__ int topk_selected_before(const TopKOrder<C> &ord, int i) {
+    if (i >= C * NT) {
+        const uint64_t m = ord.sel[C - 1][kMaxBlockWaves - 1];
+        return ord.off[C * kMaxBlockWaves - 1] + __popcll(m);
+    }
+    const int r = i / NT, t = i % NT, w = t / kWave, l = t % kWave;
+    const uint64_t below = l ? (ord.sel[r][w] & ((1ull << l) - 1)) : 0ull;
+    return ord.off[r * kMaxBlockWaves + w] + __popcll(below);
 }
 
 }  // namespace prox

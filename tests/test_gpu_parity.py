@@ -28,6 +28,12 @@ SMALL = {
     "bf16_i8_g128_640x513_b3": W.small_config(d=640, f=513, batch=3, seed=8, qbits=8),
     "bf16_i4_2048x3000_b4": W.small_config(d=2048, f=3000, batch=4, seed=9, in_frac=0.4,
                                            sigma_w=0.02),
+    # Maximum sizes: d_model 16384 (16 input rows per thread, 2 batch rows
+    # per proxy launch) and d_ff 65536 (64 score rows per thread).
+    "bf16_i4_16384x320_b3": W.small_config(d=16384, f=320, batch=3, seed=10, in_frac=0.3,
+                                           sigma_w=0.01),
+    "f16_i4_128x65536_b2": W.small_config(d=128, f=65536, batch=2, seed=12, dtype=W.DT_F16,
+                                          ff_frac=0.2),
 }
 
 

@@ -86,21 +86,17 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         }
         const uint64_t sel = topk_block<kBlock, C, true>(
             key, f, k_ff, tk, ord, [scores](int i) { return __float_as_uint(scores[i]); });
-        const int mchunk = (f + nwg - 1) / nwg;     // mask entries written by this workgroup
-        const int m_lo = w * mchunk, m_hi = m_lo + mchunk;
-#pragma unroll
-        for (int r = 0; r < C; ++r) {
-            const int i = r * kBlock + tid;
-            if (i >= f) continue;
-            const bool s = (sel >> r) & 1;
-            if (s) {
-                const int pos = topk_pos<C>(ord, r);
-                if (pos >= p0 && pos < p1) sm.list[pos - p0] = i;
-            }
-            if (i >= m_lo && i < m_hi) mask[i] = s ? 1 : 0;
+        // This workgroup's slice of positions and its chunk of the mask,
+        // straight from the order tables.
+        for (int t = tid; t < n; t += kBlock) sm.list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
+        const int mchunk = (f + nwg - 1) / nwg;   // mask entries written by this workgroup
+        const int m_lo = w * mchunk, m_hi = min(m_lo + mchunk, f);
+        for (int i = m_lo + tid; i < m_hi; i += kBlock) {
+            mask[i] = topk_is_selected<kBlock, C>(ord, i) ? 1 : 0;
+            if (scores_copy) scores_copy[i] = scores[i];
         }
-        if (scores_copy)
-            for (int i = m_lo + tid; i < min(m_hi, f); i += kBlock) scores_copy[i] = scores[i];
+        (void)sel;
+        __syncthreads();
     } else {
         for (int t = tid; t < n; t += kBlock) sm.list[t] = p0 + t;
     }

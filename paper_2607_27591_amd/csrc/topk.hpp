@@ -368,16 +368,19 @@ __device__ __forceinline__ uint64_t topk_block(const uint32_t (&key)[C], int n, 
                 }
             }
             __syncthreads();
-            if (wid == 0 && lane < bucket) {
-                const uint32_t mk = sh.cand_key[lane];
-                const int mi = sh.cand_idx[lane];
+            if (wid == 0) {
+                // Lane l holds candidate l; the others are read with readlane.
+                const bool act = lane < bucket;
+                const uint32_t mk = act ? sh.cand_key[lane] : 0u;
+                const int mi = act ? sh.cand_idx[lane] : 0;
                 int rank = 0;
                 for (int j = 0; j < bucket; ++j) {
-                    const uint32_t kj = sh.cand_key[j];
-                    const int ij = sh.cand_idx[j];
+                    const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mk, j);
+                    const int ij = __builtin_amdgcn_readlane(mi, j);
                     rank += (kj > mk || (kj == mk && ij < mi)) ? 1 : 0;
                 }
-                if (rank < kk) atomicOr(reinterpret_cast<unsigned long long *>(&selw[mi % NT]), 1ull << (mi / NT));
+                if (act && rank < kk)
+                    atomicOr(reinterpret_cast<unsigned long long *>(&selw[mi % NT]), 1ull << (mi / NT));
             }
             __syncthreads();
             sel |= selw[tid];
@@ -399,6 +402,38 @@ template <int C>
 __device__ __forceinline__ int topk_pos(const TopKOrder<C> &ord, int r) {
     const int wid = threadIdx.x / kWave;
     return ord.off[r * kMaxBlockWaves + wid] + (int)lanes_below(ord.sel[r][wid]);
+}
+
+// Index of the selected item at ascending position p (0 <= p < number
+// selected), any thread: binary search of the scanned table, then the
+// position's set bit in that (row, wave) ballot.
+template <int NT, int C>
+__device__ __forceinline__ int topk_item_at(const TopKOrder<C> &ord, int p) {
+    constexpr int E = C * kMaxBlockWaves;
+    int lo = 0, hi = E - 1;   // largest e with off[e] <= p holds p
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (ord.off[mid] <= p) lo = mid; else hi = mid - 1;
+    }
+    const int r = lo / kMaxBlockWaves, w = lo % kMaxBlockWaves;
+    uint64_t m = ord.sel[r][w];
+    int n = p - ord.off[lo];   // the n-th set bit (from 0) of m
+    int base = 0;
+#pragma unroll
+    for (int half = 32; half >= 1; half >>= 1) {
+        const uint64_t lowmask = (half == 64) ? ~0ull : ((1ull << half) - 1);
+        const int cnt = __popcll(m & lowmask);
+        if (n >= cnt) { n -= cnt; m >>= half; base += half; }
+        else m &= lowmask;
+    }
+    return r * NT + w * kWave + base;
+}
+
+// Whether item i (0 <= i < C * NT) is selected, any thread.
+template <int NT, int C>
+__device__ __forceinline__ bool topk_is_selected(const TopKOrder<C> &ord, int i) {
+    const int r = i / NT, t = i % NT;
+    return (ord.sel[r][t / kWave] >> (t % kWave)) & 1;
 }
 
 // Number of selected items with index < i (0 <= i <= C * NT), any thread.

@@ -47,8 +47,11 @@ def parse():
                     help="override the kept-channel fraction as 1 - sparsity")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--warm", action="store_true", help="headline from back-to-back calls")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized buffer 5 times (reference kernel of known "
+                         "traffic for scaling HBM counters) and exit")
     return ap.parse_args()
 
 
@@ -105,7 +108,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
-              "(the sparse decode step is single-GPU; sharding is described in DESIGN.md)",
+              "(this build runs the sparse decode step on one GPU)",
               file=sys.stderr)
         sys.exit(2)
 
@@ -117,6 +120,17 @@ def main():
     prox.lib()   # fails loudly if libprox.so is missing
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n // 8, dtype=torch.int64, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": n, "calibrate_copy_bytes_written": n,
+                          "launches": 5}), flush=True)
+        return
 
     if args.workload.startswith("c5"):
         return bench_stack(args, np, torch, prox, W, dev)
@@ -280,14 +294,16 @@ def cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes):
     cu, su = oracle.quantize(wl.w_up, cfg.dtype, cfg.qbits, cfg.group)
     n = 0
     t0 = time.perf_counter()
-    while n < len(xs_np) and (time.perf_counter() - t0) < args.cpu_budget_s:
-        oracle.ffn_sparse(xs_np[n], cfg.dtype, wl.w_gate, wl.w_up, wl.w_down, k_in, k_ff,
-                          codes_g=cg, scales_g=sg, codes_u=cu, scales_u=su, group=cfg.group)
+    # Calls on the bench's decode vectors in turn until the time budget is spent.
+    while (time.perf_counter() - t0) < args.cpu_budget_s:
+        oracle.ffn_sparse(xs_np[n % len(xs_np)], cfg.dtype, wl.w_gate, wl.w_up, wl.w_down, k_in,
+                          k_ff, codes_g=cg, scales_g=sg, codes_u=cu, scales_u=su, group=cfg.group)
         n += 1
     dt = (time.perf_counter() - t0) / max(n, 1)
     return {"value": round(total_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
             "kind": "oracle", "us_per_call": round(dt * 1e6, 1),
-            "sample": f"{n} sparse decode calls of {cfg.name} at batch {B} "
+            "sample": f"{n} sparse decode calls of {cfg.name} at batch {B} over "
+                      f"{min(n, len(xs_np))} decode vectors, {time.perf_counter() - t0:.1f} s "
                       f"(fp64 C oracle, OpenMP; proxy quantised beforehand)"}
 
 

@@ -269,34 +269,39 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     }
 }
 
-// y[b][c] = sum over workgroups (in workgroup order) of the partial y, rounded
-// once.  A block covers 64 columns; its 16 waves take interleaved workgroups
-// and are summed in wave order.
+// y[b][c] = sum over the Stage 2 workgroups of the partial y, rounded once.
+// A 256-thread block covers kReduceCols columns; thread t takes column
+// t % kReduceCols and every kReduceGroups-th workgroup from t / kReduceCols,
+// with all its loads in flight at once, and the groups are added in a fixed
+// order through LDS, so the result is deterministic.
+constexpr int kReduceThreads = 256;
+constexpr int kReduceCols = 32;
+constexpr int kReduceGroups = kReduceThreads / kReduceCols;                 // 8
+constexpr int kReducePerThread = (kStage2MaxWGs + kReduceGroups - 1) / kReduceGroups;   // 32
+
 template <int DT>
-__global__ __launch_bounds__(kBlock) void reduce_kernel(const float *__restrict__ ypart, int nwg,
-                                                        int nbt, int d, uint16_t *__restrict__ y) {
-    __shared__ float red[kMaxBlockWaves][kWave];
-    const int b = blockIdx.y, wid = threadIdx.x / kWave, lane = lane_id();
-    const int c = blockIdx.x * kWave + lane;
-    float acc = 0.0f;
-    if (c < d) {
-        constexpr int U = 8;
-        for (int w0 = wid; w0 < nwg; w0 += kMaxBlockWaves * U) {
-            float v[U];
+__global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const float *__restrict__ ypart, int nwg,
+                                                                int nbt, int d, uint16_t *__restrict__ y) {
+    __shared__ float red[kReduceGroups][kReduceCols];
+    const int b = blockIdx.y, col = threadIdx.x % kReduceCols, g = threadIdx.x / kReduceCols;
+    const int c = blockIdx.x * kReduceCols + col;
+    const int cc = min(c, d - 1);
+    float v[kReducePerThread];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int w = w0 + u * kMaxBlockWaves;
-                v[u] = w < nwg ? ypart[((size_t)w * nbt + b) * d + c] : 0.0f;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) acc += v[u];
-        }
+    for (int u = 0; u < kReducePerThread; ++u) {   // clamped loads, masked below
+        const int w = min(g + u * kReduceGroups, nwg - 1);
+        v[u] = ypart[((size_t)w * nbt + b) * d + cc];
     }
-    red[wid][lane] = acc;
+    float acc = 0.0f;
+#pragma unroll
+    for (int u = 0; u < kReducePerThread; ++u)
+        if (g + u * kReduceGroups < nwg) acc += v[u];
+    red[g][col] = acc;
     __syncthreads();
-    if (wid == 0 && c < d) {
+    if (g == 0 && c < d) {
         float s = 0.0f;
-        for (int w = 0; w < kMaxBlockWaves; ++w) s += red[w][lane];
+#pragma unroll
+        for (int q = 0; q < kReduceGroups; ++q) s += red[q][col];
         y[(size_t)b * d + c] = float_to_half<DT>(s);
     }
 }
@@ -394,12 +399,12 @@ hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const v
 
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
                          hipStream_t st) {
-    dim3 grid((d + kWave - 1) / kWave, nb);
+    dim3 grid((d + kReduceCols - 1) / kReduceCols, nb);
     const int nbt = ypart_rows(nb);
     if (dtype == kBF16)
-        reduce_kernel<kBF16><<<grid, kBlock, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
+        reduce_kernel<kBF16><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
     else
-        reduce_kernel<kF16><<<grid, kBlock, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
+        reduce_kernel<kF16><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
     return hipGetLastError();
 }
 

@@ -5,9 +5,9 @@
 // key load is coalesced.  Keys are unsigned 32-bit and order like the values
 // they stand for (magnitude patterns, non-negative IEEE floats).
 //
-// Fast path.  After a block max, every key is shifted left so that the
-// largest key's leading one sits at bit 31; the top 16 bits of the shifted
-// key (its "window") stay in registers, two per VGPR.  Two MSB-first radix
+// Fast path.  Every key is shifted left by a fixed amount so that its top 16
+// significant bits (for non-negative floats: exponent and 8 mantissa bits)
+// form its "window", kept in registers, two per VGPR.  Two MSB-first radix
 // passes with 8-bit digits find the window value w* holding the k-th largest
 // key.  When all items with window w* are needed the selection is
 // {window >= w*}; otherwise, if at most one wave's worth of items share w*,
@@ -311,20 +311,23 @@ __device__ __forceinline__ uint64_t topk_block(const uint32_t (&key)[C], int n, 
                                                TopKOrder<C> &ord, const Reload &reload) {
     static_assert(C % 2 == 0 && C <= 64, "paired windows, 64 selection bits");
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
-    // Block max (valid items), with the histogram cleared behind it.
-    uint32_t kmax = 0;
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-            if (r * NT + tid < n) kmax = max(kmax, key[r]);
-    }
+    // Fixed windows: non-negative IEEE floats (kHasLow) have bit 31 clear, so
+    // key << 1 puts the exponent and the top 8 mantissa bits in the high
+    // half; keys of at most 16 bits are the window themselves.
+    constexpr int shift = kHasLow ? 1 : 16;
     for (int b = tid; b < 256 * kHistCopies / 4; b += NT)
         reinterpret_cast<uint4 *>(sh.hist)[b] = make_uint4(0, 0, 0, 0);
-    kmax = block_max_u32<NT>(kmax, sh);
-    const int shift = kmax ? __clz(kmax) : 0;
+    __syncthreads();
     uint32_t h2[C / 2];
+    // Low key halves, two per word, kept for the tie step where registers
+    // allow (up to 32 rows); otherwise they are reloaded.
+    constexpr bool kLowRegs = kHasLow && C <= 32;
+    uint32_t l2[kLowRegs ? C / 2 : 1];
 #pragma unroll
-    for (int q = 0; q < C / 2; ++q)   // rows past n hold junk and are never read
+    for (int q = 0; q < C / 2; ++q) {   // rows past n hold junk and are never read
         h2[q] = ((key[2 * q] << shift) >> 16) | ((key[2 * q + 1] << shift) & 0xFFFF0000u);
+        if constexpr (kLowRegs) l2[q] = (key[2 * q] & 0xFFFFu) | (key[2 * q + 1] << 16);
+    }
     auto win = [&](int r) -> uint32_t { return (r & 1) ? (h2[r >> 1] >> 16) : (h2[r >> 1] & 0xFFFFu); };
     auto valid = [&](int r) { return r * NT + tid < n; };
 
@@ -363,7 +366,14 @@ __device__ __forceinline__ uint64_t topk_block(const uint32_t (&key)[C], int n, 
                 if (valid(r) && win(r) == w_star) {
                     const int i = r * NT + tid;
                     const int slot = atomicAdd(&sh.cand_n, 1);
-                    sh.cand_key[slot] = kHasLow ? reload(i) << shift : w_star << 16;
+                    uint32_t ck = w_star << 16;
+                    if constexpr (kLowRegs) {
+                        const uint32_t lo = (r & 1) ? (l2[r >> 1] >> 16) : (l2[r >> 1] & 0xFFFFu);
+                        ck |= (lo << shift) & 0xFFFFu;   // the shifted key's low half
+                    } else if constexpr (kHasLow) {
+                        ck = reload(i) << shift;
+                    }
+                    sh.cand_key[slot] = ck;
                     sh.cand_idx[slot] = i;
                 }
             }

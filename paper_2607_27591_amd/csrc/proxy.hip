@@ -146,6 +146,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     constexpr int U = (QB == 8 && NB == 4) ? 4 : 8;   // row pairs in flight per lane group
     constexpr int SZ = CPL / 8;                   // uint4 of scales per lane and group
     constexpr bool kEarlyX = NB <= 2;             // projected x loaded with the keys
+    constexpr bool kHoistX = NB == 1;             // x pairs read with the code loads
     constexpr float off = QB == 4 ? Magic<DT>::offset : 128.0f;
     using W = typename ProxyLoad<QB, CPL>::type;
     const BlobLayout L(d, f, QB, group);
@@ -323,11 +324,16 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
             // Unconditional loads (the tail repeats the last pair, with x = 0
             // below), so the compiler keeps all 2U loads in flight.
             W wa[U], wb[U];
+            // x pairs read alongside (one batch row), so their LDS latency
+            // overlaps the global loads instead of stalling each slot.
+            uint32_t xpre[kHoistX ? U : 1];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const uint32_t rr = rows32[min(p0 + u, pb - 1)];
+                const int pc = min(p0 + u, pb - 1);
+                const uint32_t rr = rows32[pc];
                 wa[u] = *reinterpret_cast<const W *>(tbase + (__umul24(rr & 0xFFFFu, rstride) + lane_off));
                 wb[u] = *reinterpret_cast<const W *>(tbase + (__umul24(rr >> 16, rstride) + lane_off));
+                if constexpr (kHoistX) xpre[u] = xs32[pc];
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -350,7 +356,9 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                     }
 #pragma unroll
                     for (int b = 0; b < NB; ++b) {
-                        const uint32_t xp = p < pb ? xs32[b * (cap / 2) + p] : 0u;
+                        uint32_t xp;
+                        if constexpr (kHoistX) xp = p < pb ? xpre[u] : 0u;
+                        else xp = p < pb ? xs32[b * (cap / 2) + p] : 0u;
                         pair_accumulate<DT, QB, CPL, (NB <= 2)>(wa[u], wb[u], xp, acc[b]);
                         xs[b] = dot2<DT>(xp, Magic<DT>::one, xs[b]);
                     }

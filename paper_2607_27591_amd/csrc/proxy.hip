@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
             const int padded = (cnt + 1) / 2 * 2;
             const int incl = wave_inclusive_scan(padded);
             if (g <= ng) gstart[g] = carry + incl - padded;
-            carry += __shfl(incl, kWave - 1, kWave);
+            carry += __builtin_amdgcn_readlane(incl, kWave - 1);
         }
     }
     __syncthreads();
@@ -369,12 +369,16 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     }
 
     // ---- combine lane groups, then waves, in a fixed order ----
+    static_assert(LPS == 8 || LPS == 16 || LPS == 32, "lane-group sizes");
 #pragma unroll
-    for (int o = LPS; o < kWave; o <<= 1)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) tot[b][e] += __shfl_xor(tot[b][e], o, kWave);
+        for (int e = 0; e < CPL; ++e) {
+            float t = tot[b][e];
+            if constexpr (LPS == 8) t += dpp_move<kDppRor8>(t);   // lane ^ 8
+            if constexpr (LPS <= 16) t = add_swap16(t);
+            tot[b][e] = add_swap32(t);
+        }
     __syncthreads();   // the list is dead; reuse the LDS for the reduction
     float *red = reinterpret_cast<float *>(dsm);   // [16][NB][2T]
     if (lane < LPS) {

@@ -51,8 +51,7 @@ struct TopKOrder {
 template <int NT>
 __device__ __forceinline__ uint32_t block_max_u32(uint32_t v, TopKScratch &sh) {
     constexpr int NW = NT / kWave;
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+    v = wave_max_u32(v);
     if (lane_id() == 0) sh.wmax[threadIdx.x / kWave] = v;
     __syncthreads();
     uint32_t m = 0;
@@ -265,8 +264,7 @@ __device__ __forceinline__ void topk_pass(const Item &item, int n, TopKScratch &
         const uint4 c4 = *h;
         *h = make_uint4(0, 0, 0, 0);
         uint32_t t = c4.x + c4.y + c4.z + c4.w;
-        t += (uint32_t)__shfl_xor((int)t, 1, kWave);
-        t += (uint32_t)__shfl_xor((int)t, 2, kWave);
+        t = quad_sum_u32(t);
         if ((tid % 4) == 0) sh.cnt[dgt] = t;
     }
     __syncthreads();

@@ -59,6 +59,19 @@ def lib():
         L.oracle_ffn_sparse.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, I, I,
                                         P, P, P, P, P]
         L.oracle_add_rmsnorm.argtypes = [P, P, I, I, I, D, P]
+        L.oracle_double_to_bf16.argtypes = [D]
+        L.oracle_double_to_bf16.restype = ctypes.c_uint16
+        L.oracle_round_to_dtype.argtypes = [P, I, I, P]
+        L.oracle_halves_to_double.argtypes = [P, I, I, P]
+        L.oracle_select_threshold.argtypes = [P, I, D, P]
+        L.oracle_select_threshold.restype = I
+        L.oracle_select_inputs_tau.argtypes = [P, I, I, I, D, P]
+        L.oracle_select_inputs_tau.restype = I
+        L.oracle_ffn_sparse_tau.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, D, D,
+                                            P, I, P, P, P, P, P]
+        L.oracle_reservoir_add.argtypes = [P, I, P, P, I, P]
+        L.oracle_quantile_threshold.argtypes = [P, I, D]
+        L.oracle_quantile_threshold.restype = D
         L.oracle_max_threads.restype = I
         _lib = L
     return _lib
@@ -196,3 +209,151 @@ def add_rmsnorm(x, y, dtype: int, eps: float = 1e-6):
 
 def max_threads() -> int:
     return int(lib().oracle_max_threads())
+
+
+# ---------------------------------------------------------------------------
+# Threshold mode (Sec. 4.1 masks with layer-wise thresholds, App. A.6) and
+# its calibration (App. A.7, Alg. 1)
+# ---------------------------------------------------------------------------
+
+def double_to_bf16(v: float) -> int:
+    """bfloat16 round-to-nearest-even of a double (bit pattern)."""
+    return int(lib().oracle_double_to_bf16(float(v)))
+
+
+def halves_to_double(bits, dtype: int):
+    """Exact values of an array of 16-bit patterns."""
+    h = _u16(bits)
+    out = np.empty(h.shape)
+    lib().oracle_halves_to_double(_p(h), h.size, dtype, _p(out))
+    return out
+
+
+def round_to_dtype(v, dtype: int):
+    """Array of doubles rounded (RNE) to the 16-bit dtype, as uint16 bits."""
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = np.empty(v.shape, np.uint16)
+    lib().oracle_round_to_dtype(_p(v), v.size, dtype, _p(out))
+    return out
+
+
+def select_threshold(key, tau: float):
+    """App. A.6 threshold rule: ascending indices with key >= tau."""
+    key = np.ascontiguousarray(key, dtype=np.float64)
+    out = np.empty(max(key.size, 1), np.int32)
+    k = lib().oracle_select_threshold(_p(key), key.size, float(tau), _p(out))
+    return out[:k].copy()
+
+
+def select_inputs_tau(x, dtype: int, tau_x: float):
+    """Sec. 4.1 input mask with a threshold: max_b |x_{b,i}| >= tau_x."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    out = np.empty(d, np.int32)
+    k = lib().oracle_select_inputs_tau(_p(x), dtype, B, d, float(tau_x), _p(out))
+    return out[:k].copy()
+
+
+def ffn_sparse_tau(x, dtype: int, w_gate, w_up, w_down, tau_x: float, tau_s: float, *,
+                   codes_g=None, scales_g=None, codes_u=None, scales_u=None, group: int = 0,
+                   kind=PROXY_QUANT, mask_override=None):
+    """Whole Sec. 4.1 decode step with thresholds.  Returns dict(y, in_idx,
+    score, ff_idx, k_in, k_ff); the counts follow from the data."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    wg, wu, wd = _u16(w_gate), _u16(w_up), _u16(w_down)
+    f = wg.shape[0]
+    if kind == PROXY_QUANT:
+        codes_g = np.ascontiguousarray(codes_g, np.int8)
+        codes_u = np.ascontiguousarray(codes_u, np.int8)
+        scales_g, scales_u = _u16(scales_g), _u16(scales_u)
+    mo = None if mask_override is None else np.ascontiguousarray(mask_override, np.int32)
+    in_idx = np.empty(d, np.int32)
+    score = np.empty(f)
+    ff_idx = np.empty(f, np.int32)
+    counts = np.zeros(2, np.int32)
+    y = np.empty((B, d))
+    lib().oracle_ffn_sparse_tau(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), kind,
+                                _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
+                                float(tau_x), float(tau_s), _p(mo), 0 if mo is None else mo.size,
+                                _p(in_idx), _p(score), _p(ff_idx), _p(counts), _p(y))
+    k_in, k_ff = int(counts[0]), int(counts[1])
+    return {"y": y, "in_idx": in_idx[:k_in].copy(), "score": score,
+            "ff_idx": ff_idx[:k_ff].copy(), "k_in": k_in, "k_ff": k_ff}
+
+
+class Reservoir:
+    """App. A.7 bounded activation sample (Algorithm R); the caller supplies
+    one uniform 64-bit random number per offered value."""
+
+    def __init__(self, cap: int):
+        self.cap = int(cap)
+        self.buf = np.zeros(self.cap)
+        self.seen = ctypes.c_longlong(0)
+
+    def add(self, values, rand_u64):
+        v = np.ascontiguousarray(values, dtype=np.float64).ravel()
+        r = np.ascontiguousarray(rand_u64, dtype=np.uint64).ravel()
+        assert r.size == v.size
+        lib().oracle_reservoir_add(_p(self.buf), self.cap, ctypes.byref(self.seen), _p(v),
+                                   v.size, _p(r))
+
+    def sample(self):
+        return self.buf[:min(self.cap, self.seen.value)].copy()
+
+
+def quantile_threshold(samples, s: float) -> float:
+    """App. A.7 threshold for target sparsity s: the ascending sample value at
+    position min(n - 1, floor(s n))."""
+    v = np.ascontiguousarray(samples, dtype=np.float64).ravel()
+    return float(lib().oracle_quantile_threshold(_p(v), v.size, float(s)))
+
+
+def stack_layer_tau(x_bits, dtype: int, layer: dict, tau_x: float, tau_s: float,
+                    eps: float = 1e-6):
+    """One layer of the stacked model with the threshold rule: y = FFN(x),
+    then x' = RMSNorm(x + y), each rounded once to the dtype.  Returns
+    (x' bits [B][d], ffn_sparse_tau result)."""
+    r = ffn_sparse_tau(x_bits, dtype, layer["w_gate"], layer["w_up"], layer["w_down"],
+                       tau_x, tau_s, codes_g=layer["codes_g"], scales_g=layer["scales_g"],
+                       codes_u=layer["codes_u"], scales_u=layer["scales_u"],
+                       group=layer["group"])
+    y_bits = round_to_dtype(r["y"], dtype)
+    xn = add_rmsnorm(x_bits, y_bits, dtype, eps)
+    return round_to_dtype(xn, dtype), r
+
+
+def calibrate_stack(tokens, dtype: int, layers, s1: float, s2: float, cap: int, draw,
+                    eps: float = 1e-6):
+    """Alg. 1 sequential threshold calibration on calibration tokens.
+
+    tokens: [T][d] bit patterns (the first layer's inputs, one token a row).
+    layers: per layer dict(w_gate, w_up, w_down, codes_g, scales_g, codes_u,
+    scales_u, group).  For each layer in depth order: collect its inputs
+    through the earlier layers run with their finalised thresholds, set
+    tau_x from |x| (target s1), build m_x per token, set tau_s from the proxy
+    |s~| computed on m_x (target s2), then finalise the layer.  Samples go
+    through a reservoir of `cap`; draw(n) returns n uniform uint64 draws.
+    Returns [(tau_x, tau_s)] per layer."""
+    xs = _u16(np.atleast_2d(tokens))
+    T, d = xs.shape
+    taus = []
+    for layer in layers:
+        res_x = Reservoir(cap)
+        for t in range(T):
+            mag = np.abs(halves_to_double(xs[t], dtype))
+            res_x.add(mag, draw(mag.size))
+        tau_x = quantile_threshold(res_x.sample(), s1)
+        res_s = Reservoir(cap)
+        for t in range(T):
+            in_idx = select_inputs_tau(xs[t], dtype, tau_x)
+            _, _, st, _ = proxy(xs[t], dtype, in_idx, codes_g=layer["codes_g"],
+                                scales_g=layer["scales_g"], codes_u=layer["codes_u"],
+                                scales_u=layer["scales_u"], group=layer["group"])
+            mag = np.abs(st[0])
+            res_s.add(mag, draw(mag.size))
+        tau_s = quantile_threshold(res_s.sample(), s2)
+        taus.append((tau_x, tau_s))
+        xs = np.stack([stack_layer_tau(xs[t], dtype, layer, tau_x, tau_s, eps)[0][0]
+                       for t in range(T)])
+    return taus

@@ -85,6 +85,45 @@ uint16_t oracle_double_to_f16(double v)
     return sign | (uint16_t)(biased << 10) | mant;
 }
 
+/* Round a double to bfloat16 (8 exponent bits as binary32, 7 fraction bits),
+ * round-to-nearest ties-to-even; returns the bit pattern. */
+uint16_t oracle_double_to_bf16(double v)
+{
+    uint16_t sign = signbit(v) ? 0x8000 : 0;
+    double a = fabs(v);
+    if (isnan(v))
+        return 0x7FC0;
+    if (a == 0.0)
+        return sign;
+    int e2;
+    frexp(a, &e2);
+    int E = e2 - 1;
+    if (E < -126)
+        E = -126;                  /* subnormals share the 2^-133 quantum */
+    double quantum = ldexp(1.0, E - 7);
+    double r = nearbyint(a / quantum) * quantum;
+    if (r >= ldexp(1.0, 128))
+        return sign | 0x7F80;
+    float fr = (float)r;           /* exact: r has at most 8 significant bits */
+    uint32_t u;
+    memcpy(&u, &fr, sizeof u);
+    return sign | (uint16_t)(u >> 16);
+}
+
+/* out[i] = the exact value of the 16-bit pattern h[i]. */
+void oracle_halves_to_double(const uint16_t *h, int n, int dtype, double *out)
+{
+    for (int i = 0; i < n; ++i)
+        out[i] = oracle_half_to_double(h[i], dtype);
+}
+
+/* out[i] = v[i] rounded to the 16-bit dtype (RNE), as bit patterns. */
+void oracle_round_to_dtype(const double *v, int n, int dtype, uint16_t *out)
+{
+    for (int i = 0; i < n; ++i)
+        out[i] = dtype == DT_BF16 ? oracle_double_to_bf16(v[i]) : oracle_double_to_f16(v[i]);
+}
+
 static double silu(double z)
 {
     /* SiLU(z) = z * sigmoid(z) = z / (1 + e^{-z})  (Sec. 2.1). */
@@ -387,6 +426,136 @@ void oracle_ffn_sparse(const uint16_t *x, int dtype, int B, int d, int f,
     free(in_idx);
     free(ff_idx);
     free(score);
+}
+
+/* ------------------------------------------------------------------ */
+/* Threshold-mode selection (Sec. 4.1 masks with layer-wise thresholds,  */
+/* App. A.6)                                                            */
+/* ------------------------------------------------------------------ */
+/* The indices i (ascending) whose key is at least tau; returns how many. */
+int oracle_select_threshold(const double *key, int n, double tau, int32_t *idx_out)
+{
+    int c = 0;
+    for (int i = 0; i < n; ++i)
+        if (key[i] >= tau)
+            idx_out[c++] = i;
+    return c;
+}
+
+/* Input mask m_x with a threshold: keep channel i when a_i = max_b |x_{b,i}|
+ * is at least tau_x (one set shared by the batch; for one row this is
+ * |x_i| >= tau_x).  in_idx must hold d entries; returns k_in. */
+int oracle_select_inputs_tau(const uint16_t *x, int dtype, int B, int d, double tau_x,
+                             int32_t *in_idx)
+{
+    double *a = (double *)malloc(sizeof(double) * (size_t)d);
+    for (int i = 0; i < d; ++i) {
+        double m = 0.0;
+        for (int b = 0; b < B; ++b) {
+            double v = fabs(XV(b, i));
+            if (v > m)
+                m = v;
+        }
+        a[i] = m;
+    }
+    int k = oracle_select_threshold(a, d, tau_x, in_idx);
+    free(a);
+    return k;
+}
+
+/*
+ * The decode step with thresholds instead of counts: m_x from tau_x, the
+ * proxy on m_x, m_s = {j : score_j >= tau_s}, Stage 2 on m_s.  The counts
+ * k_in and k_ff follow from the data.  mask_override (n_override entries,
+ * ascending) replaces m_s as in oracle_ffn_sparse.  Outputs: in_idx_out [d],
+ * score_out [f], ff_idx_out [f] (each may be NULL), counts[0] = k_in,
+ * counts[1] = k_ff, y [B][d].
+ */
+void oracle_ffn_sparse_tau(const uint16_t *x, int dtype, int B, int d, int f,
+                           const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
+                           int proxy_kind, const int8_t *cg, const uint16_t *sg,
+                           const int8_t *cu, const uint16_t *su, int group,
+                           double tau_x, double tau_s,
+                           const int32_t *mask_override, int n_override,
+                           int32_t *in_idx_out, double *score_out, int32_t *ff_idx_out,
+                           int32_t *counts, double *y)
+{
+    int32_t *in_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)d);
+    int32_t *ff_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)f);
+    double *score = (double *)malloc(sizeof(double) * (size_t)f);
+    int k_in = oracle_select_inputs_tau(x, dtype, B, d, tau_x, in_idx);
+    oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
+                 wg, wu, NULL, NULL, NULL, score);
+    int k_ff;
+    if (mask_override) {
+        memcpy(ff_idx, mask_override, sizeof(int32_t) * (size_t)n_override);
+        k_ff = n_override;
+    } else {
+        k_ff = oracle_select_threshold(score, f, tau_s, ff_idx);
+    }
+    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y);
+    if (in_idx_out)
+        memcpy(in_idx_out, in_idx, sizeof(int32_t) * (size_t)k_in);
+    if (score_out)
+        memcpy(score_out, score, sizeof(double) * (size_t)f);
+    if (ff_idx_out)
+        memcpy(ff_idx_out, ff_idx, sizeof(int32_t) * (size_t)k_ff);
+    counts[0] = k_in;
+    counts[1] = k_ff;
+    free(in_idx);
+    free(ff_idx);
+    free(score);
+}
+
+/* ------------------------------------------------------------------ */
+/* Threshold calibration (App. A.7): a bounded sample per signal and    */
+/* its empirical quantile                                               */
+/* ------------------------------------------------------------------ */
+/*
+ * Reservoir of at most cap samples over a stream (Algorithm R).  The stream
+ * item numbered t (0-based, *seen items came before this call) fills slot t
+ * while t < cap; after that it replaces slot (r mod (t + 1)) when that index
+ * is below cap.  r holds one uniform 64-bit random number per item, in
+ * stream order (the caller draws them).  *seen grows by n.
+ */
+void oracle_reservoir_add(double *res, int cap, long long *seen, const double *v, int n,
+                          const uint64_t *r)
+{
+    for (int i = 0; i < n; ++i) {
+        long long t = *seen + i;
+        if (t < cap) {
+            res[t] = v[i];
+        } else {
+            uint64_t j = r[i] % (uint64_t)(t + 1);
+            if (j < (uint64_t)cap)
+                res[j] = v[i];
+        }
+    }
+    *seen += n;
+}
+
+static int double_asc(const void *pa, const void *pb)
+{
+    double a = *(const double *)pa, b = *(const double *)pb;
+    return (a > b) - (a < b);
+}
+
+/* Threshold for a target sparsity s (0 <= s < 1) of the rule |z| >= tau:
+ * the sample value at 0-based position min(n - 1, floor(s n)) in ascending
+ * order, so that about s n of the n samples fall below it. */
+double oracle_quantile_threshold(const double *v, int n, double s)
+{
+    double *t = (double *)malloc(sizeof(double) * (size_t)n);
+    memcpy(t, v, sizeof(double) * (size_t)n);
+    qsort(t, (size_t)n, sizeof(double), double_asc);
+    long long pos = (long long)floor(s * (double)n);
+    if (pos > n - 1)
+        pos = n - 1;
+    if (pos < 0)
+        pos = 0;
+    double tau = t[pos];
+    free(t);
+    return tau;
 }
 
 /* ------------------------------------------------------------------ */

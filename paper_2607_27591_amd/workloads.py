@@ -216,6 +216,17 @@ def make_workload(cfg: FFNConfig, weights: bool = True) -> Workload:
     return Workload(cfg, wg, wu, wd, out, rng)
 
 
+def reservoir_draws(seed: int):
+    """Uniform 64-bit random numbers for the calibration reservoirs (one per
+    offered sample), from a seeded stream: returns draw(n) -> uint64 [n]."""
+    rng = np.random.default_rng([seed, 7])
+
+    def draw(n: int) -> np.ndarray:
+        return rng.integers(0, np.iinfo(np.uint64).max, size=n, dtype=np.uint64,
+                            endpoint=True)
+    return draw
+
+
 def small_config(name: str = "tiny", d: int = 256, f: int = 384, dtype: int = DT_BF16,
                  qbits: int = 4, group: int = 128, in_frac: float = 0.5,
                  ff_frac: float = 0.3, batch: int = 1, seed: int = 11,

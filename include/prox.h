@@ -147,6 +147,25 @@ prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const vo
                             float *scores, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The decode step with the paper's layer-wise thresholds in place of counts
+ * (Sec. 4.1 masks, App. A.6 rule; thresholds calibrated offline, App. A.7):
+ *   m_x = { i : max_b |x_{b,i}| >= tau_x }   (one set shared by the batch)
+ *   m_s = { j : score_j >= tau_s },  score_j = max_b |SiLU(g~_{b,j}) u~_{b,j}|
+ * Stage 1 and Stage 2 otherwise as prox_ffn_sparse.  The kept counts follow
+ * from the data and may be 0 (then y = 0) up to d_model and d_ff.
+ *   tau_x, tau_s  fp32 thresholds, not NaN (+inf keeps nothing, <= 0 keeps all)
+ *   counts   device int32 [2] output (4-byte aligned), or NULL:
+ *            counts[0] = |m_x|, counts[1] = |m_s| of this call
+ *   x, y, mask, in_mask, scores, ws, ws_bytes, stream: as prox_ffn_sparse.
+ * Comparisons are fp32: |x| exactly, the scores as the fp32 proxy computes
+ * them.  Returns PROX_ERR_INVALID for a NaN threshold or a misaligned counts.
+ */
+prox_status prox_ffn_sparse_tau(const prox_weights *w, const prox_proxy *p, const void *x,
+                                int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
+                                uint8_t *in_mask, float *scores, int32_t *counts, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/*
  * prox_ffn_sparse with timing: `events` holds PROX_SPARSE_STAGES + 1 caller-
  * created HIP events, recorded on `stream` before the first stage and after
  * each stage: (0) input top-k + proxy GEMV + score, (1) channel top-k +

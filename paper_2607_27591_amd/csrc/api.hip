@@ -2,6 +2,8 @@
 // host, workspace carving, and the launch sequence of each entry point.
 #include <prox.h>
 
+#include <cmath>
+
 #include "kernels.hpp"
 
 using namespace prox;
@@ -61,16 +63,19 @@ const char *const kStageNames[PROX_SPARSE_STAGES] = {"proxy_gemv_score",
 // (scores == NULL: every channel).
 prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, int k_ff,
                               const float *scores, uint8_t *mask, float *scores_copy, void *y,
-                              const Ws &W, hipEvent_t *events, hipStream_t stream) {
+                              const Ws &W, Select sel, hipEvent_t *events, hipStream_t stream) {
     const int d = w->d_model, f = w->d_ff, dt = w->dtype;
     const uint16_t *xb = static_cast<const uint16_t *>(x);
-    const int nwg = stage2_wgs(scores ? k_ff : f);
+    // With the threshold rule the kept count is found on the device: size the
+    // grid for every channel (workgroups past the count get no channels).
+    const int nwg = stage2_wgs(scores && !sel.tau_mode ? k_ff : f);
     const int ystride = ypart_rows(batch);
     for (int c0 = 0; c0 < batch; c0 += kStage2MaxNB) {
         const int nb = batch - c0 < kStage2MaxNB ? batch - c0 : kStage2MaxNB;
         PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, w->w_gate, w->w_up, w->w_down,
                                scores, k_ff, mask, c0 == 0 ? scores_copy : nullptr,
-                               W.ypart + (size_t)c0 * d, ystride, nwg, stream));
+                               W.ypart + (size_t)c0 * d, ystride, nwg,
+                               c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
     PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));
@@ -78,10 +83,17 @@ prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, i
     return PROX_OK;
 }
 
+// The selection of each stage: counts (k_in, k_ff) or thresholds.
+struct Rules {
+    int tau_mode;
+    float tau_x, tau_s;
+    int32_t *counts;   // threshold mode: [k_in, k_ff] realised, or NULL
+};
+
 prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
-                        int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
-                        float *scores, void *ws, size_t ws_bytes, hipEvent_t *events,
-                        hipStream_t stream) {
+                        int k_in, int k_ff, const Rules &rules, void *y, uint8_t *mask,
+                        uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                        hipEvent_t *events, hipStream_t stream) {
     prox_status st = check_weights(w);
     if (st != PROX_OK) return st;
     if (!p || !p->blob || !x || !y || !mask || !ws) return PROX_ERR_INVALID;
@@ -90,7 +102,14 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
         return PROX_ERR_INVALID;
     const int d = w->d_model, f = w->d_ff;
     if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
-    if (k_in < 1 || k_in > d || k_ff < 1 || k_ff > f) return PROX_ERR_INVALID;
+    if (rules.tau_mode) {
+        if (std::isnan(rules.tau_x) || std::isnan(rules.tau_s)) return PROX_ERR_INVALID;
+        if (rules.counts && !aligned(rules.counts, 4)) return PROX_ERR_INVALID;
+        k_in = d;   // the proxy's list capacity
+        k_ff = 0;
+    } else if (k_in < 1 || k_in > d || k_ff < 1 || k_ff > f) {
+        return PROX_ERR_INVALID;
+    }
     if (!proxy_shape_ok(d, p->fmt, p->group)) return PROX_ERR_UNSUPPORTED;
     const int qbits = qbits_of(p->fmt);
     if (p->bytes < BlobLayout(d, f, qbits, p->group).total) return PROX_ERR_WORKSPACE;
@@ -105,11 +124,14 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
     const int pnb = proxy_max_nb(d);
     for (int c0 = 0; c0 < batch; c0 += pnb) {
         const int nb = batch - c0 < pnb ? batch - c0 : pnb;
+        const Select in_sel{rules.tau_mode, rules.tau_x, rules.counts};
         PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
-                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, stream));
+                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[1], stream));
-    return stage2_and_reduce(w, x, batch, k_ff, W.scores, mask, scores, y, W, events, stream);
+    const Select ff_sel{rules.tau_mode, rules.tau_s, rules.counts ? rules.counts + 1 : nullptr};
+    return stage2_and_reduce(w, x, batch, k_ff, W.scores, mask, scores, y, W, ff_sel, events,
+                             stream);
 }
 
 }  // namespace
@@ -178,14 +200,23 @@ prox_status prox_ffn_dense(const prox_weights *w, const void *x, int batch, void
     const int d = w->d_model, f = w->d_ff;
     if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
     const Ws W = carve(ws, d, f, batch);
-    return stage2_and_reduce(w, x, batch, f, nullptr, nullptr, nullptr, y, W, nullptr, stream);
+    return stage2_and_reduce(w, x, batch, f, nullptr, nullptr, nullptr, y, W,
+                             Select{0, 0.0f, nullptr}, nullptr, stream);
 }
 
 prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
                             int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
                             float *scores, void *ws, size_t ws_bytes, hipStream_t stream) {
-    return sparse_impl(w, p, x, batch, k_in, k_ff, y, mask, in_mask, scores, ws, ws_bytes,
-                       nullptr, stream);
+    return sparse_impl(w, p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y, mask,
+                       in_mask, scores, ws, ws_bytes, nullptr, stream);
+}
+
+prox_status prox_ffn_sparse_tau(const prox_weights *w, const prox_proxy *p, const void *x,
+                                int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
+                                uint8_t *in_mask, float *scores, int32_t *counts, void *ws,
+                                size_t ws_bytes, hipStream_t stream) {
+    return sparse_impl(w, p, x, batch, 0, 0, Rules{1, tau_x, tau_s, counts}, y, mask, in_mask,
+                       scores, ws, ws_bytes, nullptr, stream);
 }
 
 prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, const void *x,
@@ -193,8 +224,8 @@ prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, c
                                    uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
                                    hipEvent_t *events, hipStream_t stream) {
     if (!events) return PROX_ERR_INVALID;
-    return sparse_impl(w, p, x, batch, k_in, k_ff, y, mask, in_mask, scores, ws, ws_bytes, events,
-                       stream);
+    return sparse_impl(w, p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y, mask,
+                       in_mask, scores, ws, ws_bytes, events, stream);
 }
 
 prox_status prox_add_rmsnorm(const void *x, const void *y, int batch, int d_model,

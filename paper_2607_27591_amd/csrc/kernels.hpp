@@ -15,20 +15,23 @@ hipError_t launch_unpack(int qbits, const void *blob, int d, int f, int group, i
                          uint16_t *sg, int8_t *cu, uint16_t *su, hipStream_t stream);
 
 // Stage 1 for batch rows [row0, row0 + nb) of x_all (nb <= proxy_max_nb(d));
-// the input top-k ranks all B_all rows.  accumulate != 0 keeps
+// the input selection ranks all B_all rows (top k_in, or the threshold rule
+// of sel, for which k_in is the list capacity).  accumulate != 0 keeps
 // max(previous, new) scores.
 int proxy_max_nb(int d);
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,
-                        uint8_t *in_mask, float *scores, int accumulate, hipStream_t stream);
+                        uint8_t *in_mask, float *scores, int accumulate, Select sel,
+                        hipStream_t stream);
 
 // Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
-// the dense FFN over all f channels.  Partial y rows go to
+// the dense FFN over all f channels; otherwise the top k_ff scores, or the
+// threshold rule of sel, pick the channels.  Partial y rows go to
 // ypart[(w * ystride + b) * d + c] for workgroup w < nwg.
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
                          uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, hipStream_t stream);
+                         int nwg, Select sel, hipStream_t stream);
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
                          hipStream_t stream);
 hipError_t launch_add_rmsnorm(int dtype, const void *x, const void *y, int batch, int d, float eps,

@@ -99,6 +99,15 @@ __host__ __device__ inline int ypart_rows(int batch) {
                                  : (batch + kStage2MaxNB - 1) / kStage2MaxNB * kStage2MaxNB;
 }
 
+// How a launch selects its set (Sec. 4.1 masks): by count (the top-k reading,
+// App. A.6) or, with tau_mode, by the layer-wise threshold rule |z| >= tau,
+// whose realised count then goes to *count (when count is not NULL).
+struct Select {
+    int tau_mode;
+    float tau;
+    int32_t *count;
+};
+
 // ---------------------------------------------------------------------------
 // Workspace (no initialisation needed)
 // ---------------------------------------------------------------------------

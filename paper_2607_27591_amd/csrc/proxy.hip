@@ -137,7 +137,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     int row0, int nb,                                 // rows [row0, row0 + nb) are projected
     int d, int f, int group, int k_in, const uint8_t *__restrict__ blob,
     uint8_t *__restrict__ in_mask, float *__restrict__ scores,
-    int accumulate) {
+    int accumulate, Select sel_rule) {   // k_in: the list capacity when sel_rule.tau_mode
     constexpr int CPL = proxy_cols<NB, QB>();
     constexpr int LPS = 2 * T / CPL;              // lanes per row segment (gate + up)
     constexpr int NGRP = kWave / LPS;             // lane groups per wave
@@ -196,7 +196,21 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
             }
         }
     }
-    const uint64_t sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+    uint64_t sel = 0;
+    if (sel_rule.tau_mode) {
+        // Threshold rule: keep row i when max_b |x_{b,i}| >= tau_x, compared
+        // as floats (exact for the 16-bit magnitudes).
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
+            sel |= (uint64_t)in << r;
+        }
+        topk_order<kBlock, C>(sel, d, tk, ord);
+        if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
+            *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
+    } else {
+        sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+    }
 
     // ---- group bookkeeping: kept rows per group and padded list starts ----
     for (int g = tid; g <= ng; g += kBlock) gsel0[g] = topk_selected_before<kBlock, C>(ord, g * group);
@@ -411,7 +425,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
 template <int NB, int DT, int QB, int T, int C>
 static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                  int group, int k_in, const void *blob,
-                                 uint8_t *in_mask, float *scores, int accumulate, hipStream_t s) {
+                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
     const BlobLayout L(d, f, QB, group);
     const size_t lds = proxy_lds_bytes(k_in, d / group, NB, T);
     if (lds > 65536) {
@@ -422,7 +436,7 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
     }
     proxy_kernel<NB, DT, QB, T, C><<<L.n_tiles, kBlock, lds, s>>>(
         static_cast<const uint16_t *>(x_all), B_all, row0, nb, d, f, group, k_in,
-        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate);
+        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel_rule);
     return hipGetLastError();
 }
 
@@ -430,42 +444,42 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
 template <int NB, int DT, int QB, int T>
 static hipError_t launch_proxy_c(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                  int group, int k_in, const void *blob,
-                                 uint8_t *in_mask, float *scores, int accumulate, hipStream_t s) {
+                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
     if (d <= 8 * kBlock)
-        return launch_proxy_t<NB, DT, QB, T, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-    return launch_proxy_t<NB, DT, QB, T, 16>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
+        return launch_proxy_t<NB, DT, QB, T, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+    return launch_proxy_t<NB, DT, QB, T, 16>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
 }
 
 template <int DT, int QB, int T>
 static hipError_t launch_proxy_nb(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                   int group, int k_in, const void *blob,
-                                  uint8_t *in_mask, float *scores, int accumulate, hipStream_t s) {
+                                  uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
     switch (proxy_nb_t(nb)) {
-        case 1: return launch_proxy_c<1, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-        case 2: return launch_proxy_c<2, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-        default: return launch_proxy_c<4, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
+        case 1: return launch_proxy_c<1, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+        case 2: return launch_proxy_c<2, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+        default: return launch_proxy_c<4, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
     }
 }
 
 template <int DT, int QB>
 static hipError_t launch_proxy_tile(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                     int group, int k_in, const void *blob,
-                                    uint8_t *in_mask, float *scores, int accumulate,
+                                    uint8_t *in_mask, float *scores, int accumulate, Select sel_rule,
                                     hipStream_t s) {
     if (proxy_tile(f) == 128)
-        return launch_proxy_nb<DT, QB, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-    return launch_proxy_nb<DT, QB, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
+        return launch_proxy_nb<DT, QB, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+    return launch_proxy_nb<DT, QB, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
 }
 
 int proxy_max_nb(int d) { return d <= 8192 ? kProxyMaxNB : 2; }
 
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,
-                        uint8_t *in_mask, float *scores, int accumulate, hipStream_t s) {
-    if (dtype == kBF16 && qbits == 4) return launch_proxy_tile<kBF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-    if (dtype == kBF16) return launch_proxy_tile<kBF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-    if (qbits == 4) return launch_proxy_tile<kF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
-    return launch_proxy_tile<kF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, s);
+                        uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
+    if (dtype == kBF16 && qbits == 4) return launch_proxy_tile<kBF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+    if (dtype == kBF16) return launch_proxy_tile<kBF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+    if (qbits == 4) return launch_proxy_tile<kF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+    return launch_proxy_tile<kF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
 }
 
 }  // namespace prox

@@ -61,13 +61,16 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const uint16_t *__restrict__ wu, const uint16_t *__restrict__ wd,
     const float *__restrict__ scores,   // NULL: dense FFN over all f channels
     int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
-    float *__restrict__ ypart, int ypart_stride) {   // partial y rows per workgroup
+    float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
+    Select sel_rule) {
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
-    const int n_ch = sparse ? k_ff : f;
-    const int p0 = (int)((long long)w * n_ch / nwg), p1 = (int)((long long)(w + 1) * n_ch / nwg);
-    const int n = p1 - p0;   // channels of this workgroup
+    // Channels of this workgroup: an even share of the n_ch kept channels
+    // (with the threshold rule n_ch is only known after the selection).
+    int n_ch = sparse ? k_ff : f;
+    int p0 = (int)((long long)w * n_ch / nwg), p1 = (int)((long long)(w + 1) * n_ch / nwg);
+    int n = p1 - p0;
 
     __shared__ TopKScratch tk;
     __shared__ TopKOrder<C> ord;
@@ -84,8 +87,26 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         for (int r = 0; r < C; ++r) {
             key[r] = __float_as_uint(scores[min(r * kBlock + tid, f - 1)]);
         }
-        const uint64_t sel = topk_block<kBlock, C, true>(
-            key, f, k_ff, tk, ord, [scores](int i) { return __float_as_uint(scores[i]); });
+        uint64_t sel = 0;
+        if (sel_rule.tau_mode) {
+            // Threshold rule: keep channel j when score_j >= tau_s.
+#pragma unroll
+            for (int r = 0; r < C; ++r)
+                sel |= (uint64_t)(r * kBlock + tid < f && __uint_as_float(key[r]) >= sel_rule.tau) << r;
+            topk_order<kBlock, C>(sel, f, tk, ord);
+            n_ch = topk_selected_before<kBlock, C>(ord, C * kBlock);
+            // Split over the workgroups a launch for this count would have
+            // (the grid is sized for every channel; the rest get none), so
+            // the partial sums are those of the top-k launch with k = n_ch.
+            const int nwg_k = min(nwg, stage2_wgs(n_ch));
+            p0 = w < nwg_k ? (int)((long long)w * n_ch / nwg_k) : n_ch;
+            p1 = w < nwg_k ? (int)((long long)(w + 1) * n_ch / nwg_k) : n_ch;
+            n = p1 - p0;
+            if (w == 0 && tid == 0 && sel_rule.count) *sel_rule.count = n_ch;
+        } else {
+            sel = topk_block<kBlock, C, true>(
+                key, f, k_ff, tk, ord, [scores](int i) { return __float_as_uint(scores[i]); });
+        }
         // This workgroup's slice of positions and its chunk of the mask,
         // straight from the order tables.
         for (int t = tid; t < n; t += kBlock) sm.list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
@@ -351,14 +372,14 @@ template <int NB, int DT, int C>
 static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
                                   uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, hipStream_t st) {
+                                  int ystride, int nwg, Select sel_rule, hipStream_t st) {
     const size_t lds = stage2_lds_bytes(d, NB);
     hipError_t e = allow_lds(stage2_kernel<NB, DT, C>, lds);
     if (e != hipSuccess) return e;
     stage2_kernel<NB, DT, C><<<nwg, kBlock, lds, st>>>(
         static_cast<const uint16_t *>(x), nb, d, f, static_cast<const uint16_t *>(wg),
         static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff,
-        mask, scores_copy, ypart, ystride);
+        mask, scores_copy, ypart, ystride, sel_rule);
     return hipGetLastError();
 }
 
@@ -366,28 +387,28 @@ template <int NB, int DT>
 static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
                                   uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, hipStream_t st) {
+                                  int ystride, int nwg, Select sel_rule, hipStream_t st) {
     // C = score rows per thread of the channel top-k (the dense path has none).
     if (!scores || f <= 16 * kBlock)
         return launch_stage2_t<NB, DT, 16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, st);
+                                           scores_copy, ypart, ystride, nwg, sel_rule, st);
     if (f <= 32 * kBlock)
         return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, st);
+                                           scores_copy, ypart, ystride, nwg, sel_rule, st);
     return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                       scores_copy, ypart, ystride, nwg, st);
+                                       scores_copy, ypart, ystride, nwg, sel_rule, st);
 }
 
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
                          uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, hipStream_t st) {
+                         int nwg, Select sel_rule, hipStream_t st) {
 #define S2(NB_)                                                                                    \
     return dtype == kBF16                                                                          \
                ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,    \
-                                             scores_copy, ypart, ystride, nwg, st)                 \
+                                             scores_copy, ypart, ystride, nwg, sel_rule, st)                 \
                : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,     \
-                                            scores_copy, ypart, ystride, nwg, st)
+                                            scores_copy, ypart, ystride, nwg, sel_rule, st)
     switch (stage2_nb_t(nb)) {
         case 1: S2(1);
         case 2: S2(2);

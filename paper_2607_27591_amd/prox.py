@@ -66,13 +66,14 @@ def lib() -> ctypes.CDLL:
         L.prox_ffn_dense.argtypes = [WP, P, I, P, P, S, P]
         L.prox_ffn_sparse.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P]
         L.prox_ffn_sparse_staged.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
+        L.prox_ffn_sparse_tau.argtypes = [WP, PP, P, I, Z, Z, P, P, P, P, P, P, S, P]
         L.prox_sparse_stage_name.argtypes = [I]
         L.prox_sparse_stage_name.restype = ctypes.c_char_p
         L.prox_add_rmsnorm.argtypes = [P, P, I, I, I, Z, P, P]
         L.prox_strerror.argtypes = [I]
         L.prox_strerror.restype = ctypes.c_char_p
         for name in ("prox_pack_proxy", "prox_unpack_proxy", "prox_ffn_dense", "prox_ffn_sparse",
-                     "prox_ffn_sparse_staged", "prox_add_rmsnorm"):
+                     "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -243,6 +244,34 @@ def ffn_sparse(w: Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int, *,
         arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
         _check(lib().prox_ffn_sparse_staged(*args, arr, _stream(dev)), "prox_ffn_sparse_staged")
     return y, mask
+
+
+def ffn_sparse_tau(w: Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau_s: float, *,
+                   y: Optional[torch.Tensor] = None, mask: Optional[torch.Tensor] = None,
+                   in_mask: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                   counts: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Prox decode step with layer-wise thresholds (keep |x| >= tau_x and
+    score >= tau_s).  Returns (y, mask, counts) with counts an int32 [2]
+    device tensor (k_in, k_ff realised by this call)."""
+    x = _as_batch(x, w)
+    B = x.shape[0]
+    dev = x.device
+    y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", w.dtype)
+    mask = (torch.empty(w.d_ff, dtype=torch.uint8, device=dev) if mask is None
+            else _dev_tensor(mask, "mask", torch.uint8))
+    counts = (torch.empty(2, dtype=torch.int32, device=dev) if counts is None
+              else _dev_tensor(counts, "counts", torch.int32))
+    if in_mask is not None:
+        _dev_tensor(in_mask, "in_mask", torch.uint8)
+    if scores is not None:
+        _dev_tensor(scores, "scores", torch.float32)
+    ws = new_workspace(w.d_model, w.d_ff, B, dev) if ws is None else ws
+    wst, pst = w.struct(), p.struct()
+    _check(lib().prox_ffn_sparse_tau(ctypes.byref(wst), ctypes.byref(pst), _ptr(x), B,
+                                     float(tau_x), float(tau_s), _ptr(y), _ptr(mask),
+                                     _ptr(in_mask), _ptr(scores), _ptr(counts), _ptr(ws),
+                                     ws.numel(), _stream(dev)), "prox_ffn_sparse_tau")
+    return y, mask, counts
 
 
 def add_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-6,

@@ -28,8 +28,8 @@ def _declared():
 
 def test_header_declares_the_boundary():
     names = _declared()
-    for must in ["prox_pack_proxy", "prox_ffn_dense", "prox_ffn_sparse", "prox_proxy_bytes",
-                 "prox_workspace_bytes", "prox_strerror"]:
+    for must in ["prox_pack_proxy", "prox_ffn_dense", "prox_ffn_sparse", "prox_ffn_sparse_tau",
+                 "prox_proxy_bytes", "prox_workspace_bytes", "prox_strerror"]:
         assert must in names
 
 
@@ -113,6 +113,25 @@ def test_sparse_rejects_bad_arguments():
                              1 << 40, None) == INVALID
     assert L.prox_ffn_sparse_staged(ctypes.byref(w), ctypes.byref(p), FAKE, 1, 1, 1, FAKE, FAKE,
                                     None, None, FAKE, 1 << 40, None, None) == INVALID
+
+
+def test_sparse_tau_rejects_bad_arguments():
+    L = prox.lib()
+    w, p = _weights(), _proxy()
+    nan = float("nan")
+
+    def call(tau_x=0.5, tau_s=0.1, B=1, counts=None, mask=FAKE, ws_bytes=1 << 40):
+        return L.prox_ffn_sparse_tau(ctypes.byref(w), ctypes.byref(p), FAKE, B, tau_x, tau_s,
+                                     FAKE, mask, None, None, counts, FAKE, ws_bytes, None)
+
+    assert call(tau_x=nan) == INVALID
+    assert call(tau_s=nan) == INVALID
+    assert call(counts=MISALIGNED) == INVALID
+    assert call(B=0) == INVALID
+    assert call(B=17) == INVALID
+    assert call(mask=None) == INVALID
+    assert call(ws_bytes=10) == WORKSPACE
+    assert call(tau_x=float("inf"), ws_bytes=10) == WORKSPACE   # +inf is a valid threshold
 
 
 def test_dense_pack_norm_reject_bad_arguments():

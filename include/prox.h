@@ -181,6 +181,32 @@ prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, c
 const char *prox_sparse_stage_name(int i);
 
 /*
+ * Threshold calibration (App. A.7), host code only (no HIP calls; all
+ * pointers are host memory).  Offline, a layer's thresholds come from
+ * calibration activations run through the earlier layers with their final
+ * thresholds (Alg. 1): each signal (|x| for tau_x, |s~| = the proxy scores
+ * of one token for tau_s) is kept in a bounded sample, and the threshold is
+ * that sample's empirical quantile at the target sparsity.
+ *
+ * prox_reservoir_add: offers values[0..n) to a reservoir of capacity cap
+ * (Algorithm R).  *seen counts the values offered before this call and grows
+ * by n; the reservoir holds min(cap, *seen) values.  Offer number t fills
+ * slot t while t < cap, then replaces slot (draws[i] mod (t + 1)) when that
+ * index is below cap.  draws: one uniform 64-bit random number per value,
+ * drawn by the caller.  PROX_ERR_INVALID for NULL pointers (values/draws may
+ * be NULL when n == 0) or cap == 0.
+ *
+ * prox_quantile_threshold: *tau = the sample value at ascending position
+ * min(n - 1, floor(sparsity * n)), so that about sparsity * n of the n
+ * samples lie below it and the rule |z| >= tau keeps the rest.
+ * PROX_ERR_INVALID for n == 0, sparsity outside [0, 1), a NaN sample or NULL
+ * pointers.
+ */
+prox_status prox_reservoir_add(float *reservoir, size_t cap, uint64_t *seen, const float *values,
+                               size_t n, const uint64_t *draws);
+prox_status prox_quantile_threshold(const float *samples, size_t n, double sparsity, float *tau);
+
+/*
  * Residual + unit-gain RMSNorm between stacked FFN layers:
  *   out_b = r_b / sqrt(mean(r_b^2) + eps),  r_b = x_b + y_b  (fp32),
  * rounded once to the dtype.  x, y, out: device [batch][d_model]; out may

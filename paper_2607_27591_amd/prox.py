@@ -67,13 +67,16 @@ def lib() -> ctypes.CDLL:
         L.prox_ffn_sparse.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P]
         L.prox_ffn_sparse_staged.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
         L.prox_ffn_sparse_tau.argtypes = [WP, PP, P, I, Z, Z, P, P, P, P, P, P, S, P]
+        L.prox_reservoir_add.argtypes = [P, S, P, P, S, P]
+        L.prox_quantile_threshold.argtypes = [P, S, ctypes.c_double, P]
         L.prox_sparse_stage_name.argtypes = [I]
         L.prox_sparse_stage_name.restype = ctypes.c_char_p
         L.prox_add_rmsnorm.argtypes = [P, P, I, I, I, Z, P, P]
         L.prox_strerror.argtypes = [I]
         L.prox_strerror.restype = ctypes.c_char_p
         for name in ("prox_pack_proxy", "prox_unpack_proxy", "prox_ffn_dense", "prox_ffn_sparse",
-                     "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm"):
+                     "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm",
+                     "prox_reservoir_add", "prox_quantile_threshold"):
             getattr(L, name).restype = I
         _lib = L
     return _lib

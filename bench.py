@@ -47,6 +47,9 @@ def parse():
                     help="override the kept-channel fraction as 1 - sparsity")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-tau", action="store_true", help="skip the threshold-mode leg")
+    ap.add_argument("--calib-tokens", type=int, default=32,
+                    help="held-out synthetic vectors for the threshold calibration")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--warm", action="store_true", help="headline from back-to-back calls")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -243,6 +246,11 @@ def main():
                 "frac": round(s2_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": s2_bytes, "avg_launch_us": round(s2_us, 2)}
 
+    tau = None
+    if not args.no_tau:
+        tau = threshold_leg(args, cfg, wl, w, proxy, xs, n_x, B, ws, y, mask, flush, sink,
+                            k_in, k_ff, dense_us, np, torch, prox, W, dev)
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes)
@@ -282,8 +290,61 @@ def main():
         "setup_s": round(gen_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "threshold_mode": tau,
     }
     print(json.dumps(out), flush=True)
+
+
+def threshold_leg(args, cfg, wl, w, proxy, xs, n_x, B, ws, y, mask, flush, sink, k_in, k_ff,
+                  dense_us, np, torch, prox, W, dev):
+    """The paper's threshold rule on the same workload: tau_x, tau_s from the
+    sequential calibration (one layer here) on held-out synthetic vectors at
+    the top-k leg's sparsities, then the same cold protocol on the same
+    decode vectors.  Counts are data-dependent, so bytes use each call's own
+    realised k_in, k_ff."""
+    from paper_2607_27591_amd import calibrate as C
+    s1, s2 = 1 - k_in / cfg.d_model, 1 - k_ff / cfg.d_ff
+    cal_np = wl.x_vectors(args.calib_tokens, 1)[:, 0, :]
+    cal = prox.from_bits(cal_np, cfg.dtype, dev)
+    t0 = time.perf_counter()
+    (tau_x, tau_s), = C.calibrate_stack([(w, proxy)], cal, s1, s2, 200000,
+                                        W.reservoir_draws(cfg.seed))
+    cal_s = time.perf_counter() - t0
+    counts = torch.zeros((args.steps, 2), dtype=torch.int32, device=dev)
+
+    def call(i):
+        prox.ffn_sparse_tau(w, proxy, xs[i % n_x], tau_x, tau_s, y=y, mask=mask,
+                            counts=counts[i % args.steps], ws=ws)
+
+    for i in range(args.warmup):
+        call(i)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        if not args.warm:
+            torch.sum(flush, 0, out=sink)
+        evs[i][0].record()
+        call(i)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    us = [a.elapsed_time(b) * 1e3 for a, b in evs]
+    cnt = counts.cpu().numpy()
+    byts = [sum(algorithmic_bytes(cfg, B, int(a), int(b)).values()) for a, b in cnt]
+    mean = statistics.mean(us)
+    return {"rule": "keep |x| >= tau_x and score >= tau_s (layer-wise thresholds)",
+            "tau_x": tau_x, "tau_s": tau_s,
+            "calibration": f"Alg. 1 on {args.calib_tokens} held-out synthetic vectors, "
+                           f"reservoir 200000, targets s1={s1:.4f} s2={s2:.4f}, {cal_s:.1f} s",
+            "us_per_call": {"mean": round(mean, 2), "median": round(statistics.median(us), 2),
+                            "p10": round(pct(us, 0.1), 2), "p90": round(pct(us, 0.9), 2)},
+            "k_in": {"mean": round(float(cnt[:, 0].mean()), 1), "min": int(cnt[:, 0].min()),
+                     "max": int(cnt[:, 0].max())},
+            "k_ff": {"mean": round(float(cnt[:, 1].mean()), 1), "min": int(cnt[:, 1].min()),
+                     "max": int(cnt[:, 1].max())},
+            "algorithmic_gbs": round(statistics.mean(byts) / (mean * 1e-6) / 1e9, 1),
+            "speedup_vs_dense": None if dense_us is None
+            else round(dense_us / statistics.median(us), 3)}
 
 
 def cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes):
@@ -358,6 +419,9 @@ def bench_stack(args, np, torch, prox, W, dev):
         b.record()
         torch.cuda.synchronize()
         dense_us = a.elapsed_time(b) * 1e3 / args.steps
+    tau = None
+    if not args.no_tau:
+        tau = stack_threshold_leg(args, cfg, layers, x0, y, mask, ws, L, np, torch, prox, W, dev)
     ab = sum(algorithmic_bytes(cfg, 1, cfg.k_in, cfg.k_ff).values()) * L
     mean = statistics.mean(us)
     gbs = ab / (mean * 1e-6) / 1e9
@@ -372,8 +436,48 @@ def bench_stack(args, np, torch, prox, W, dev):
                None if dense_us is None else round(dense_us, 1),
            "speedup_vs_dense": None if dense_us is None else round(dense_us / mean, 3),
            "protocol": "back-to-back tokens (12.7 GB of weights per token exceed the caches)",
-           "wall_ms_timed_region": round(wall_ms, 1), "setup_s": round(gen_s, 1)}
+           "wall_ms_timed_region": round(wall_ms, 1), "setup_s": round(gen_s, 1),
+           "threshold_mode": tau}
     print(json.dumps(out), flush=True)
+
+
+def stack_threshold_leg(args, cfg, layers, x0, y, mask, ws, L, np, torch, prox, W, dev):
+    """The stack with per-layer thresholds from Alg. 1 (sequential, each layer
+    calibrated on inputs that passed through the finished earlier layers) on
+    held-out synthetic tokens, then timed per token like the top-k stack."""
+    from paper_2607_27591_amd import calibrate as C
+    s1, s2 = 1 - cfg.k_in / cfg.d_model, 1 - cfg.k_ff / cfg.d_ff
+    cal = prox.from_bits(W.make_workload(cfg, weights=False).x_vectors(
+        1 + args.calib_tokens, 1)[1:, 0, :], cfg.dtype, dev)
+    t0 = time.perf_counter()
+    taus = C.calibrate_stack(layers, cal, s1, s2, 200000, W.reservoir_draws(cfg.seed))
+    cal_s = time.perf_counter() - t0
+    counts = torch.zeros((L, 2), dtype=torch.int32, device=dev)
+    x = torch.empty_like(x0)
+
+    def token():
+        x.copy_(x0)
+        for l, ((w, p), (tx, ts)) in enumerate(zip(layers, taus)):
+            prox.ffn_sparse_tau(w, p, x, tx, ts, y=y, mask=mask, counts=counts[l], ws=ws)
+            prox.add_rmsnorm(x, y, 1e-6, out=x)
+
+    for _ in range(args.warmup):
+        token()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(args.steps):
+        token()
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / args.steps
+    cnt = counts.cpu().numpy()
+    return {"us_per_token": round(us, 1), "tokens_per_s": round(1e6 / us, 1),
+            "calibration": f"Alg. 1 over {L} layers on {args.calib_tokens} held-out synthetic "
+                           f"tokens, reservoir 200000, s1={s1:.4f} s2={s2:.4f}, {cal_s:.1f} s",
+            "k_in_mean": round(float(cnt[:, 0].mean()), 1),
+            "k_ff_mean": round(float(cnt[:, 1].mean()), 1),
+            "k_ff_range": [int(cnt[:, 1].min()), int(cnt[:, 1].max())]}
 
 
 if __name__ == "__main__":

@@ -207,6 +207,23 @@ prox_status prox_reservoir_add(float *reservoir, size_t cap, uint64_t *seen, con
 prox_status prox_quantile_threshold(const float *samples, size_t n, double sparsity, float *tau);
 
 /*
+ * Sparsity allocation between the two stages (Sec. 4.2), host code only.
+ * A dense FFN costs 3 (one per projection); a proxy projection costs alpha
+ * (the paper rounds its measured ratios to 1/3).
+ *
+ * prox_effective_sparsity: e = 1 - (2 alpha (1 - s1) + 3 (1 - s2)) / 3.
+ *
+ * prox_allocate_sparsity: (s1, s2) for a target e.  s2 = s_ref (the paper
+ * uses 0.7) and s1 takes the remaining budget; if that s1 leaves
+ * [s1_min, s1_max] (the paper uses [0, 0.7]) it is clamped to the nearer
+ * bound and s2 is solved again from e.  PROX_ERR_INVALID for alpha <= 0,
+ * s1_min > s1_max, a NaN argument or a NULL output.
+ */
+double prox_effective_sparsity(double s1, double s2, double alpha);
+prox_status prox_allocate_sparsity(double e, double alpha, double s_ref, double s1_min,
+                                   double s1_max, double *s1, double *s2);
+
+/*
  * Residual + unit-gain RMSNorm between stacked FFN layers:
  *   out_b = r_b / sqrt(mean(r_b^2) + eps),  r_b = x_b + y_b  (fp32),
  * rounded once to the dtype.  x, y, out: device [batch][d_model]; out may

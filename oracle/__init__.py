@@ -72,6 +72,11 @@ def lib():
         L.oracle_reservoir_add.argtypes = [P, I, P, P, I, P]
         L.oracle_quantile_threshold.argtypes = [P, I, D]
         L.oracle_quantile_threshold.restype = D
+        L.oracle_prox_cost.argtypes = [D, D, D]
+        L.oracle_prox_cost.restype = D
+        L.oracle_effective_sparsity.argtypes = [D, D, D]
+        L.oracle_effective_sparsity.restype = D
+        L.oracle_allocate.argtypes = [D, D, D, D, D, P, P]
         L.oracle_max_threads.restype = I
         _lib = L
     return _lib
@@ -357,3 +362,25 @@ def calibrate_stack(tokens, dtype: int, layers, s1: float, s2: float, cap: int, 
         xs = np.stack([stack_layer_tau(xs[t], dtype, layer, tau_x, tau_s, eps)[0][0]
                        for t in range(T)])
     return taus
+
+
+# ---------------------------------------------------------------------------
+# Cost model and sparsity allocation (Sec. 4.2)
+# ---------------------------------------------------------------------------
+
+def prox_cost(s1: float, s2: float, alpha: float = 1.0 / 3.0) -> float:
+    """Sec. 4.2 normalised cost (a dense FFN costs 3)."""
+    return float(lib().oracle_prox_cost(s1, s2, alpha))
+
+
+def effective_sparsity(s1: float, s2: float, alpha: float = 1.0 / 3.0) -> float:
+    """Sec. 4.2 effective sparsity against the dense FFN."""
+    return float(lib().oracle_effective_sparsity(s1, s2, alpha))
+
+
+def allocate(e: float, alpha: float = 1.0 / 3.0, s_ref: float = 0.7, s1_min: float = 0.0,
+             s1_max: float = 0.7):
+    """Sec. 4.2 allocation of a target effective sparsity: (s1, s2)."""
+    a, b = ctypes.c_double(), ctypes.c_double()
+    lib().oracle_allocate(e, alpha, s_ref, s1_min, s1_max, ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value

@@ -559,6 +559,41 @@ double oracle_quantile_threshold(const double *v, int n, double s)
 }
 
 /* ------------------------------------------------------------------ */
+/* Cost model and sparsity allocation (Sec. 4.2)                        */
+/* ------------------------------------------------------------------ */
+/* Normalised cost: each dense projection costs 1 (a dense FFN costs 3); a
+ * proxy projection costs alpha.  Stage 1 runs two proxy projections on a
+ * (1 - s1) share of the inputs, Stage 2 three exact projections on a
+ * (1 - s2) share of the channels. */
+double oracle_prox_cost(double s1, double s2, double alpha)
+{
+    return 2.0 * alpha * (1.0 - s1) + 3.0 * (1.0 - s2);
+}
+
+/* Effective sparsity against the dense cost of 3. */
+double oracle_effective_sparsity(double s1, double s2, double alpha)
+{
+    return 1.0 - oracle_prox_cost(s1, s2, alpha) / 3.0;
+}
+
+/* Allocation for a target effective sparsity e: s2 starts at s_ref and s1
+ * takes the rest of the budget; when that s1 leaves [s1_min, s1_max] it is
+ * clamped to the nearer bound and s2 is solved again from e. */
+void oracle_allocate(double e, double alpha, double s_ref, double s1_min, double s1_max,
+                     double *s1_out, double *s2_out)
+{
+    double s2 = s_ref;
+    /* e = s2 - 2 alpha (1 - s1) / 3  =>  s1 = 1 - 3 (s2 - e) / (2 alpha) */
+    double s1 = 1.0 - 3.0 * (s2 - e) / (2.0 * alpha);
+    if (s1 < s1_min || s1 > s1_max) {
+        s1 = s1 < s1_min ? s1_min : s1_max;
+        s2 = e + 2.0 * alpha * (1.0 - s1) / 3.0;
+    }
+    *s1_out = s1;
+    *s2_out = s2;
+}
+
+/* ------------------------------------------------------------------ */
 /* Residual + RMSNorm between stacked layers (unit gain)                */
 /* ------------------------------------------------------------------ */
 /* out_b = r_b / sqrt(mean(r_b^2) + eps),  r_b = x_b + y_b.  out is [B][d]. */

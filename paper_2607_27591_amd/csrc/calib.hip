@@ -42,4 +42,30 @@ prox_status prox_quantile_threshold(const float *samples, size_t n, double spars
     return PROX_OK;
 }
 
+// Sec. 4.2 cost model: a dense projection costs 1 and a proxy projection
+// alpha; Stage 1 runs two proxy projections over the kept (1 - s1) inputs,
+// Stage 2 three exact ones over the kept (1 - s2) channels.
+double prox_effective_sparsity(double s1, double s2, double alpha) {
+    const double cost = 2.0 * alpha * (1.0 - s1) + 3.0 * (1.0 - s2);
+    return 1.0 - cost / 3.0;   // against the dense cost of 3
+}
+
+prox_status prox_allocate_sparsity(double e, double alpha, double s_ref, double s1_min,
+                                   double s1_max, double *s1, double *s2) {
+    if (!s1 || !s2 || !(alpha > 0.0) || !(s1_min <= s1_max) || std::isnan(e) ||
+        std::isnan(s_ref) || std::isnan(s1_min) || std::isnan(s1_max))
+        return PROX_ERR_INVALID;
+    // Stage 2 at its anchor, Stage 1 takes the rest of the budget; a Stage 1
+    // share outside its bounds is clamped and Stage 2 solved again.
+    double b = s_ref;
+    double a = 1.0 - 1.5 * (b - e) / alpha;
+    if (a < s1_min || a > s1_max) {
+        a = std::min(std::max(a, s1_min), s1_max);
+        b = e + 2.0 * alpha * (1.0 - a) / 3.0;
+    }
+    *s1 = a;
+    *s2 = b;
+    return PROX_OK;
+}
+
 }  // extern "C"

@@ -69,6 +69,10 @@ def lib() -> ctypes.CDLL:
         L.prox_ffn_sparse_tau.argtypes = [WP, PP, P, I, Z, Z, P, P, P, P, P, P, S, P]
         L.prox_reservoir_add.argtypes = [P, S, P, P, S, P]
         L.prox_quantile_threshold.argtypes = [P, S, ctypes.c_double, P]
+        Dd = ctypes.c_double
+        L.prox_effective_sparsity.argtypes = [Dd, Dd, Dd]
+        L.prox_effective_sparsity.restype = Dd
+        L.prox_allocate_sparsity.argtypes = [Dd, Dd, Dd, Dd, Dd, P, P]
         L.prox_sparse_stage_name.argtypes = [I]
         L.prox_sparse_stage_name.restype = ctypes.c_char_p
         L.prox_add_rmsnorm.argtypes = [P, P, I, I, I, Z, P, P]
@@ -76,7 +80,7 @@ def lib() -> ctypes.CDLL:
         L.prox_strerror.restype = ctypes.c_char_p
         for name in ("prox_pack_proxy", "prox_unpack_proxy", "prox_ffn_dense", "prox_ffn_sparse",
                      "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm",
-                     "prox_reservoir_add", "prox_quantile_threshold"):
+                     "prox_reservoir_add", "prox_quantile_threshold", "prox_allocate_sparsity"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -275,6 +279,21 @@ def ffn_sparse_tau(w: Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau_s: f
                                      _ptr(in_mask), _ptr(scores), _ptr(counts), _ptr(ws),
                                      ws.numel(), _stream(dev)), "prox_ffn_sparse_tau")
     return y, mask, counts
+
+
+def effective_sparsity(s1: float, s2: float, alpha: float = 1.0 / 3.0) -> float:
+    """Sec. 4.2 effective sparsity of stage sparsities (s1, s2)."""
+    return float(lib().prox_effective_sparsity(float(s1), float(s2), float(alpha)))
+
+
+def allocate_sparsity(e: float, alpha: float = 1.0 / 3.0, s_ref: float = 0.7,
+                      s1_min: float = 0.0, s1_max: float = 0.7):
+    """Sec. 4.2 allocation of a target effective sparsity: (s1, s2)."""
+    a, b = ctypes.c_double(), ctypes.c_double()
+    _check(lib().prox_allocate_sparsity(float(e), float(alpha), float(s_ref), float(s1_min),
+                                        float(s1_max), ctypes.byref(a), ctypes.byref(b)),
+           "prox_allocate_sparsity")
+    return a.value, b.value
 
 
 def add_rmsnorm(x: torch.Tensor, y: torch.Tensor, eps: float = 1e-6,

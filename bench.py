@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-tau", action="store_true", help="skip the threshold-mode leg")
+    ap.add_argument("--alpha", action="store_true",
+                    help="measure the proxy-cost ratio alpha (quantised over 16-bit proxy)")
     ap.add_argument("--calib-tokens", type=int, default=32,
                     help="held-out synthetic vectors for the threshold calibration")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
@@ -137,6 +139,8 @@ def main():
 
     if args.workload.startswith("c5"):
         return bench_stack(args, np, torch, prox, W, dev)
+    if args.alpha:
+        return bench_alpha(args, np, torch, prox, W, dev)
 
     cfg = W.CONFIGS[args.workload]
     B = args.batch or cfg.batch
@@ -345,6 +349,56 @@ def threshold_leg(args, cfg, wl, w, proxy, xs, n_x, B, ws, y, mask, flush, sink,
             "algorithmic_gbs": round(statistics.mean(byts) / (mean * 1e-6) / 1e9, 1),
             "speedup_vs_dense": None if dense_us is None
             else round(dense_us / statistics.median(us), 3)}
+
+
+def bench_alpha(args, np, torch, prox, W, dev):
+    """Sec. 4.2 proxy-cost ratio alpha on this GPU: the Stage 1 time with the
+    workload's quantised proxy over the time with the unquantised 16-bit
+    proxy (PROX_Q_NONE), at the same input sparsity, cold.  Stage 1 is the
+    proxy kernel between the staged entry point's events.  Its input
+    selection is the same for both formats."""
+    cfg = W.CONFIGS[args.workload]
+    wl = W.make_workload(cfg)
+    w = prox.Weights(*(prox.from_bits(m, cfg.dtype, dev) for m in (wl.w_gate, wl.w_up, wl.w_down)))
+    fmt = prox.INT4 if cfg.qbits == 4 else prox.INT8
+    proxies = {"quant": prox.pack_proxy(w, fmt, cfg.group), "none": prox.pack_proxy(w, prox.NONE)}
+    n_x = 8
+    xs = prox.from_bits(wl.x_vectors(n_x, 1)[:, 0, :], cfg.dtype, dev)
+    ws = prox.new_workspace(cfg.d_model, cfg.d_ff, 1, dev)
+    y = torch.empty((1, cfg.d_model), dtype=w.dtype, device=dev)
+    mask = torch.empty(cfg.d_ff, dtype=torch.uint8, device=dev)
+    flush = torch.ones(FLUSH_BYTES // 8, dtype=torch.int64, device=dev)
+    sink = torch.zeros((), dtype=torch.int64, device=dev)
+    rows = []
+    for s1 in (0.0, 0.1, 0.55, 0.7):
+        k_in = max(1, W.frac_to_k(1.0 - s1, cfg.d_model))
+        med = {}
+        for name, p in proxies.items():
+            stage = [[torch.cuda.Event(enable_timing=True) for _ in range(prox.SPARSE_STAGES + 1)]
+                     for _ in range(args.steps)]
+            for row in stage:
+                for ev in row:
+                    ev.record()
+            for i in range(args.warmup):
+                prox.ffn_sparse(w, p, xs[i % n_x], k_in, cfg.k_ff, y=y, mask=mask, ws=ws)
+            torch.cuda.synchronize()
+            for i in range(args.steps):
+                torch.sum(flush, 0, out=sink)
+                prox.ffn_sparse(w, p, xs[i % n_x], k_in, cfg.k_ff, y=y, mask=mask, ws=ws,
+                                events=stage[i])
+            torch.cuda.synchronize()
+            med[name] = statistics.median(r[0].elapsed_time(r[1]) * 1e3 for r in stage)
+        rows.append({"input_sparsity": s1, "k_in": k_in, "quant_us": round(med["quant"], 2),
+                     "none_us": round(med["none"], 2),
+                     "alpha": round(med["quant"] / med["none"], 3)})
+    alphas = [r["alpha"] for r in rows]
+    out = {"metric": "proxy-cost ratio alpha (Stage 1 time, quantised over 16-bit proxy)",
+           "value": round(statistics.mean(alphas), 3), "unit": "ratio", "n_gpus": 1,
+           "higher_is_better": False, "config": {"workload": cfg.name,
+           "proxy": f"int{cfg.qbits} group {cfg.group} vs unquantised {W.DTYPE_NAMES[cfg.dtype]}"},
+           "rows": rows, "protocol": "cold, median of the staged proxy-stage time",
+           "paper_alpha": 1.0 / 3.0}
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes):

@@ -42,7 +42,11 @@ typedef enum {
 
 typedef enum { PROX_F16 = 0, PROX_BF16 = 1 } prox_dtype;
 
-typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1 } prox_qfmt;
+/* Proxy formats.  PROX_Q_NONE keeps W_gate, W_up themselves, in the weights'
+ * 16-bit dtype (the unquantised-proxy ablation, W~ = W; also the reference
+ * point of the proxy-cost ratio alpha of Sec. 4.2); it takes group = d_model
+ * and has no codes to unpack. */
+typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1, PROX_Q_NONE = 2 } prox_qfmt;
 
 /* Supported sizes. */
 #define PROX_MAX_BATCH 16

@@ -19,9 +19,12 @@ bool shape_ok(int d, int f) {
            f <= PROX_MAX_D_FF;
 }
 
-int qbits_of(int fmt) { return fmt == PROX_Q_INT4 ? 4 : fmt == PROX_Q_INT8 ? 8 : 0; }
+int qbits_of(int fmt) {
+    return fmt == PROX_Q_INT4 ? 4 : fmt == PROX_Q_INT8 ? 8 : fmt == PROX_Q_NONE ? 16 : 0;
+}
 
 bool proxy_shape_ok(int d, int fmt, int group) {
+    if (fmt == PROX_Q_NONE) return group == d;   // one unit scale per channel
     return qbits_of(fmt) != 0 && group >= 128 && group % 128 == 0 && d % group == 0;
 }
 
@@ -182,7 +185,8 @@ prox_status prox_unpack_proxy(const prox_proxy *p, int d_model, int d_ff, int8_t
         return PROX_ERR_INVALID;
     if (!aligned(p->blob, 16) || !aligned(scales_gate, 2) || !aligned(scales_up, 2))
         return PROX_ERR_INVALID;
-    if (!shape_ok(d_model, d_ff) || !proxy_shape_ok(d_model, p->fmt, p->group))
+    if (!shape_ok(d_model, d_ff) || !proxy_shape_ok(d_model, p->fmt, p->group) ||
+        p->fmt == PROX_Q_NONE)
         return PROX_ERR_UNSUPPORTED;
     const int qbits = qbits_of(p->fmt);
     if (p->bytes < BlobLayout(d_model, d_ff, qbits, p->group).total) return PROX_ERR_WORKSPACE;

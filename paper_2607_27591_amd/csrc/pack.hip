@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
     const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid == 0) {
         BlobHeader h{};
-        h.magic = kBlobMagic; h.version = kBlobVersion; h.fmt = QB == 4 ? 1u : 0u;
+        h.magic = kBlobMagic; h.version = kBlobVersion; h.fmt = QB == 4 ? 1u : QB == 8 ? 0u : 2u;
         h.group = (uint32_t)group; h.d_model = (uint32_t)d; h.d_ff = (uint32_t)f;
         h.tile = (uint32_t)L.tile; h.qbits = QB;
         h.codes_offset = L.codes_offset; h.scales_offset = L.scales_offset;
@@ -68,6 +68,21 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint16_t *__restrict__ 
     constexpr int qmax = QB == 4 ? 7 : 127;
     const int T = L.tile;
     const int tile = j0 / T, c0 = j0 % T;
+    if constexpr (QB == 16) {
+        // Unquantised proxy: the weights' own 16-bit patterns, unit scales.
+        uint16_t *scales = reinterpret_cast<uint16_t *>(blob + L.scales_offset);
+        const size_t sb = (((size_t)tile * ng + g) * 2 + mat) * T + c0;
+        scales[sb] = 0x3C00u;   // fp16 1.0
+        scales[sb + 1] = 0x3C00u;
+        for (int ii = 0; ii < group; ++ii) {
+            const int i = g * group + ii;
+            uint16_t *seg = reinterpret_cast<uint16_t *>(blob + L.codes_offset + (size_t)i * L.row_stride +
+                                                         (size_t)tile * L.row_bytes);
+            seg[mat * T + c0] = j0 < f ? w[(size_t)j0 * d + i] : (uint16_t)0;
+            seg[mat * T + c0 + 1] = j0 + 1 < f ? w[(size_t)(j0 + 1) * d + i] : (uint16_t)0;
+        }
+        return;
+    }
 
     double sigma[2];
     uint16_t sbits[2];
@@ -151,9 +166,11 @@ hipError_t launch_pack(int dtype, int qbits, const void *wg, const void *wu, int
     auto *u = static_cast<const uint16_t *>(wu);
     auto *b = static_cast<uint8_t *>(blob);
     if (dtype == kBF16 && qbits == 4) pack_kernel<kBF16, 4><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
-    else if (dtype == kBF16) pack_kernel<kBF16, 8><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
+    else if (dtype == kBF16 && qbits == 8) pack_kernel<kBF16, 8><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
+    else if (dtype == kBF16) pack_kernel<kBF16, 16><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
     else if (qbits == 4) pack_kernel<kF16, 4><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
-    else pack_kernel<kF16, 8><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
+    else if (qbits == 8) pack_kernel<kF16, 8><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
+    else pack_kernel<kF16, 16><<<nb, 256, 0, s>>>(g, u, d, f, group, b);
     return hipGetLastError();
 }
 

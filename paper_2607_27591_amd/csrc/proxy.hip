@@ -11,10 +11,11 @@
 // padded per quantisation group to an even count.  Each lane group then
 // streams a contiguous range of row pairs.
 //
-// A lane reads 4 (INT4) or 8 (INT8) bytes of both rows' contiguous segments,
-// i.e. the same 8 proxy columns of two input rows.  For INT4 the two rows'
-// bytes are interleaved with v_perm and each nibble pair is OR-ed under the
-// exponent of 128.0 (bf16) or 1024.0 (fp16): that is the exact 16-bit pair
+// A lane reads 4 (INT4), 8 (INT8) or 16 (unquantised 16-bit proxy) bytes of
+// both rows' contiguous segments, i.e. the same 8 proxy columns of two input
+// rows.  For INT4 the two rows' bytes are interleaved with v_perm and each
+// nibble pair is OR-ed under the exponent of 128.0 (bf16) or 1024.0 (fp16):
+// that is the exact 16-bit pair
 // (M + n_a, M + n_b), n = q + 8, and one dot2 accumulates
 // x_a (M + n_a) + x_b (M + n_b) in fp32.  (M + 8) * sum(x) is subtracted and
 // the group's scale applied once per group, column and lane group.  Lane groups and waves
@@ -113,6 +114,7 @@ template <> struct ProxyLoad<4, 16> { using type = uint2; };
 template <> struct ProxyLoad<4, 8> { using type = uint32_t; };
 template <> struct ProxyLoad<8, 16> { using type = uint4; };
 template <> struct ProxyLoad<8, 8> { using type = uint2; };
+template <> struct ProxyLoad<16, 8> { using type = uint4; };   // unquantised 16-bit proxy
 
 template <int DT, int QB, int CPL, bool FUSED>
 __device__ __forceinline__ void pair_accumulate(const typename ProxyLoad<QB, CPL>::type &a,
@@ -123,11 +125,19 @@ __device__ __forceinline__ void pair_accumulate(const typename ProxyLoad<QB, CPL
         int4_pair_dot8<DT, FUSED>(a.y, b.y, xp, acc + 8);
     } else if constexpr (QB == 4) {
         int4_pair_dot8<DT, FUSED>(a, b, xp, acc);
-    } else if constexpr (CPL == 16) {
+    } else if constexpr (QB == 8 && CPL == 16) {
         int8_pair_fma8<DT>(make_uint2(a.x, a.y), make_uint2(b.x, b.y), xp, acc);
         int8_pair_fma8<DT>(make_uint2(a.z, a.w), make_uint2(b.z, b.w), xp, acc + 8);
-    } else {
+    } else if constexpr (QB == 8) {
         int8_pair_fma8<DT>(a, b, xp, acc);
+    } else {
+        // 16-bit weights: (w_a[c], w_b[c]) side by side, one dot2 with (x_a, x_b).
+        const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc[2 * q] = dot2<DT>(xp, __builtin_amdgcn_perm(bw[q], aw[q], 0x05040100u), acc[2 * q]);
+            acc[2 * q + 1] = dot2<DT>(xp, __builtin_amdgcn_perm(bw[q], aw[q], 0x07060302u), acc[2 * q + 1]);
+        }
     }
 }
 
@@ -143,11 +153,11 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     constexpr int NGRP = kWave / LPS;             // lane groups per wave
     constexpr int NLG = kMaxBlockWaves * NGRP;    // lane groups per workgroup
     static_assert(C * kBlock <= kMaxDModel, "input rows per thread");
-    constexpr int U = (QB == 8 && NB == 4) ? 4 : 8;   // row pairs in flight per lane group
+    constexpr int U = ((QB == 8 && NB == 4) || QB == 16) ? 4 : 8;   // row pairs in flight per lane group
     constexpr int SZ = CPL / 8;                   // uint4 of scales per lane and group
     constexpr bool kEarlyX = NB <= 2;             // projected x loaded with the keys
     constexpr bool kHoistX = NB == 1;             // x pairs read with the code loads
-    constexpr float off = QB == 4 ? Magic<DT>::offset : 128.0f;
+    constexpr float off = QB == 4 ? Magic<DT>::offset : QB == 8 ? 128.0f : 0.0f;   // code bias
     using W = typename ProxyLoad<QB, CPL>::type;
     const BlobLayout L(d, f, QB, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
@@ -476,10 +486,10 @@ int proxy_max_nb(int d) { return d <= 8192 ? kProxyMaxNB : 2; }
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,
                         uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
-    if (dtype == kBF16 && qbits == 4) return launch_proxy_tile<kBF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-    if (dtype == kBF16) return launch_proxy_tile<kBF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-    if (qbits == 4) return launch_proxy_tile<kF16, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-    return launch_proxy_tile<kF16, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+#define PX(DT_, QB_) launch_proxy_tile<DT_, QB_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s)
+    if (dtype == kBF16) return qbits == 4 ? PX(kBF16, 4) : qbits == 8 ? PX(kBF16, 8) : PX(kBF16, 16);
+    return qbits == 4 ? PX(kF16, 4) : qbits == 8 ? PX(kF16, 8) : PX(kF16, 16);
+#undef PX
 }
 
 }  // namespace prox

@@ -17,7 +17,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libprox.so")
 
 F16, BF16 = 0, 1
-INT8, INT4 = 0, 1
+INT8, INT4, NONE = 0, 1, 2   # NONE: unquantised 16-bit proxy (group = d_model)
 MAX_BATCH = 16
 SPARSE_STAGES = 3
 
@@ -176,6 +176,8 @@ def new_workspace(d_model: int, d_ff: int, batch: int, device="cuda") -> torch.T
 
 
 def pack_proxy(w: Weights, fmt: int = INT4, group: int = 128) -> Proxy:
+    if fmt == NONE:
+        group = w.d_model   # the unquantised proxy has one unit scale per channel
     n = proxy_bytes(w.d_model, w.d_ff, fmt, group)
     if n == 0:
         raise ProxError(2, "prox_proxy_bytes")

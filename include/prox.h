@@ -42,6 +42,12 @@ typedef enum {
 
 typedef enum { PROX_F16 = 0, PROX_BF16 = 1 } prox_dtype;
 
+/* Gate activation: SwiGLU (SiLU(z) = z / (1 + e^-z), Sec. 2.1) or GeGLU
+ * (GELU(z) = z * Phi(z) = z (1 + erf(z / sqrt 2)) / 2, the gated FFN of the
+ * Gemma models the paper mentions).  Applied to the proxy (Stage 1) and to
+ * the exact gate (Stage 2) alike. */
+typedef enum { PROX_ACT_SILU = 0, PROX_ACT_GELU = 1 } prox_act;
+
 /* Proxy formats.  PROX_Q_NONE keeps W_gate, W_up themselves, in the weights'
  * 16-bit dtype (the unquantised-proxy ablation, W~ = W; also the reference
  * point of the proxy-cost ratio alpha of Sec. 4.2); it takes group = d_model
@@ -71,6 +77,7 @@ typedef struct {
     const void *w_gate;
     const void *w_up;
     const void *w_down;
+    prox_act act;   /* PROX_ACT_SILU unless the FFN is a GeGLU */
 } prox_weights;
 
 /*

@@ -22,6 +22,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 PROXY_QUANT = 0   # W~ from codes/scales
 PROXY_NONE = 1    # W~ = W (unquantised proxy)
+SILU, GELU = 0, 1  # gate activation: SwiGLU (Sec. 2.1) or GeGLU
 
 
 def build(force: bool = True) -> str:
@@ -52,12 +53,12 @@ def lib():
         L.oracle_quantize.argtypes = [P, I, I, I, I, I, P, P]
         L.oracle_topk.argtypes = [P, I, I, P]
         L.oracle_select_inputs.argtypes = [P, I, I, I, I, P]
-        L.oracle_proxy.argtypes = [P, I, I, I, I, P, I, I, P, P, P, P, I, P, P, P, P, P, P]
+        L.oracle_proxy.argtypes = [P, I, I, I, I, P, I, I, P, P, P, P, I, P, P, P, P, P, P, I]
         L.oracle_select_channels.argtypes = [P, I, I, P]
-        L.oracle_stage2.argtypes = [P, I, I, I, I, P, P, P, P, I, P, P]
-        L.oracle_ffn_dense.argtypes = [P, I, I, I, I, P, P, P, P]
+        L.oracle_stage2.argtypes = [P, I, I, I, I, P, P, P, P, I, P, P, I]
+        L.oracle_ffn_dense.argtypes = [P, I, I, I, I, P, P, P, P, I]
         L.oracle_ffn_sparse.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, I, I,
-                                        P, P, P, P, P]
+                                        P, P, P, P, P, I]
         L.oracle_add_rmsnorm.argtypes = [P, P, I, I, I, D, P]
         L.oracle_double_to_bf16.argtypes = [D]
         L.oracle_double_to_bf16.restype = ctypes.c_uint16
@@ -68,7 +69,9 @@ def lib():
         L.oracle_select_inputs_tau.argtypes = [P, I, I, I, D, P]
         L.oracle_select_inputs_tau.restype = I
         L.oracle_ffn_sparse_tau.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, D, D,
-                                            P, I, P, P, P, P, P]
+                                            P, I, P, P, P, P, P, I]
+        L.oracle_gate_act.argtypes = [D, I]
+        L.oracle_gate_act.restype = D
         L.oracle_reservoir_add.argtypes = [P, I, P, P, I, P]
         L.oracle_quantile_threshold.argtypes = [P, I, D]
         L.oracle_quantile_threshold.restype = D
@@ -129,7 +132,7 @@ def select_inputs(x, dtype: int, k_in: int):
 
 
 def proxy(x, dtype: int, in_idx, *, codes_g=None, scales_g=None, codes_u=None,
-          scales_u=None, group: int = 0, w_gate=None, w_up=None, kind=PROXY_QUANT):
+          scales_u=None, group: int = 0, w_gate=None, w_up=None, kind=PROXY_QUANT, act=SILU):
     """Sec. 4.1 Stage 1: returns (g~ [B][f], u~ [B][f], s~ [B][f], score [f])."""
     x = _u16(np.atleast_2d(x))
     B, d = x.shape
@@ -145,7 +148,7 @@ def proxy(x, dtype: int, in_idx, *, codes_g=None, scales_g=None, codes_u=None,
     gt = np.empty((B, f)); ut = np.empty((B, f)); st = np.empty((B, f)); sc = np.empty(f)
     lib().oracle_proxy(_p(x), dtype, B, d, f, _p(in_idx), in_idx.size, kind,
                        _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
-                       _p(w_gate), _p(w_up), _p(gt), _p(ut), _p(st), _p(sc))
+                       _p(w_gate), _p(w_up), _p(gt), _p(ut), _p(st), _p(sc), act)
     return gt, ut, st, sc
 
 
@@ -154,7 +157,7 @@ def select_channels(score, k_ff: int):
     return topk(score, k_ff)
 
 
-def stage2(x, dtype: int, w_gate, w_up, w_down, ff_idx):
+def stage2(x, dtype: int, w_gate, w_up, w_down, ff_idx, act=SILU):
     """Sec. 4.1 Stage 2 on channels ff_idx: returns (s [B][k_ff], y [B][d])."""
     x = _u16(np.atleast_2d(x))
     B, d = x.shape
@@ -164,23 +167,23 @@ def stage2(x, dtype: int, w_gate, w_up, w_down, ff_idx):
     s = np.empty((B, max(ff_idx.size, 1)))
     y = np.empty((B, d))
     lib().oracle_stage2(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), _p(ff_idx),
-                        ff_idx.size, _p(s), _p(y))
+                        ff_idx.size, _p(s), _p(y), act)
     return s[:, :ff_idx.size], y
 
 
-def ffn_dense(x, dtype: int, w_gate, w_up, w_down):
+def ffn_dense(x, dtype: int, w_gate, w_up, w_down, act=SILU):
     """Sec. 2.1 dense SwiGLU FFN in fp64: y [B][d]."""
     x = _u16(np.atleast_2d(x))
     B, d = x.shape
     wg, wu, wd = _u16(w_gate), _u16(w_up), _u16(w_down)
     y = np.empty((B, d))
-    lib().oracle_ffn_dense(_p(x), dtype, B, d, wg.shape[0], _p(wg), _p(wu), _p(wd), _p(y))
+    lib().oracle_ffn_dense(_p(x), dtype, B, d, wg.shape[0], _p(wg), _p(wu), _p(wd), _p(y), act)
     return y
 
 
 def ffn_sparse(x, dtype: int, w_gate, w_up, w_down, k_in: int, k_ff: int, *,
                codes_g=None, scales_g=None, codes_u=None, scales_u=None, group: int = 0,
-               kind=PROXY_QUANT, mask_override=None):
+               kind=PROXY_QUANT, mask_override=None, act=SILU):
     """Whole Sec. 4.1 decode step.  Returns dict(y, in_idx, score, ff_idx)."""
     x = _u16(np.atleast_2d(x))
     B, d = x.shape
@@ -199,7 +202,7 @@ def ffn_sparse(x, dtype: int, w_gate, w_up, w_down, k_in: int, k_ff: int, *,
     y = np.empty((B, d))
     lib().oracle_ffn_sparse(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), kind,
                             _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
-                            k_in, k_ff, _p(mo), _p(in_idx), _p(score), _p(ff_idx), _p(y))
+                            k_in, k_ff, _p(mo), _p(in_idx), _p(score), _p(ff_idx), _p(y), act)
     return {"y": y, "in_idx": in_idx, "score": score, "ff_idx": ff_idx}
 
 
@@ -261,7 +264,7 @@ def select_inputs_tau(x, dtype: int, tau_x: float):
 
 def ffn_sparse_tau(x, dtype: int, w_gate, w_up, w_down, tau_x: float, tau_s: float, *,
                    codes_g=None, scales_g=None, codes_u=None, scales_u=None, group: int = 0,
-                   kind=PROXY_QUANT, mask_override=None):
+                   kind=PROXY_QUANT, mask_override=None, act=SILU):
     """Whole Sec. 4.1 decode step with thresholds.  Returns dict(y, in_idx,
     score, ff_idx, k_in, k_ff); the counts follow from the data."""
     x = _u16(np.atleast_2d(x))
@@ -281,7 +284,7 @@ def ffn_sparse_tau(x, dtype: int, w_gate, w_up, w_down, tau_x: float, tau_s: flo
     lib().oracle_ffn_sparse_tau(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), kind,
                                 _p(codes_g), _p(scales_g), _p(codes_u), _p(scales_u), group,
                                 float(tau_x), float(tau_s), _p(mo), 0 if mo is None else mo.size,
-                                _p(in_idx), _p(score), _p(ff_idx), _p(counts), _p(y))
+                                _p(in_idx), _p(score), _p(ff_idx), _p(counts), _p(y), act)
     k_in, k_ff = int(counts[0]), int(counts[1])
     return {"y": y, "in_idx": in_idx[:k_in].copy(), "score": score,
             "ff_idx": ff_idx[:k_ff].copy(), "k_in": k_in, "k_ff": k_ff}
@@ -322,7 +325,7 @@ def stack_layer_tau(x_bits, dtype: int, layer: dict, tau_x: float, tau_s: float,
     r = ffn_sparse_tau(x_bits, dtype, layer["w_gate"], layer["w_up"], layer["w_down"],
                        tau_x, tau_s, codes_g=layer["codes_g"], scales_g=layer["scales_g"],
                        codes_u=layer["codes_u"], scales_u=layer["scales_u"],
-                       group=layer["group"])
+                       group=layer["group"], act=layer.get("act", SILU))
     y_bits = round_to_dtype(r["y"], dtype)
     xn = add_rmsnorm(x_bits, y_bits, dtype, eps)
     return round_to_dtype(xn, dtype), r
@@ -354,7 +357,8 @@ def calibrate_stack(tokens, dtype: int, layers, s1: float, s2: float, cap: int, 
             in_idx = select_inputs_tau(xs[t], dtype, tau_x)
             _, _, st, _ = proxy(xs[t], dtype, in_idx, codes_g=layer["codes_g"],
                                 scales_g=layer["scales_g"], codes_u=layer["codes_u"],
-                                scales_u=layer["scales_u"], group=layer["group"])
+                                scales_u=layer["scales_u"], group=layer["group"],
+                                act=layer.get("act", SILU))
             mag = np.abs(st[0])
             res_s.add(mag, draw(mag.size))
         tau_s = quantile_threshold(res_s.sample(), s2)
@@ -384,3 +388,8 @@ def allocate(e: float, alpha: float = 1.0 / 3.0, s_ref: float = 0.7, s1_min: flo
     a, b = ctypes.c_double(), ctypes.c_double()
     lib().oracle_allocate(e, alpha, s_ref, s1_min, s1_max, ctypes.byref(a), ctypes.byref(b))
     return a.value, b.value
+
+
+def gate_act(z: float, act: int) -> float:
+    """Gate activation: SiLU (SwiGLU, Sec. 2.1) or GELU z Phi(z) (GeGLU)."""
+    return float(lib().oracle_gate_act(float(z), int(act)))

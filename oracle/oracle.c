@@ -130,6 +130,20 @@ static double silu(double z)
     return z / (1.0 + exp(-z));
 }
 
+/* GELU(z) = z * Phi(z), Phi the standard normal CDF = erfc(-z / sqrt 2) / 2
+ * (= (1 + erf(z / sqrt 2)) / 2, without the cancellation for z << 0): the
+ * gate of a GeGLU FFN. */
+static double gelu(double z)
+{
+    return 0.5 * z * erfc(-z / sqrt(2.0));
+}
+
+/* Gate activation of the gated FFN: 0 SiLU (SwiGLU), 1 GELU (GeGLU). */
+double oracle_gate_act(double z, int act)
+{
+    return act == 0 ? silu(z) : gelu(z);
+}
+
 #define XV(b, i) oracle_half_to_double(x[(size_t)(b) * d + (i)], dtype)
 #define WV(w, j, i) oracle_half_to_double((w)[(size_t)(j) * d + (i)], dtype)
 
@@ -253,7 +267,7 @@ void oracle_proxy(const uint16_t *x, int dtype, int B, int d, int f,
                   const int8_t *cg, const uint16_t *sg,
                   const int8_t *cu, const uint16_t *su, int group,
                   const uint16_t *wg, const uint16_t *wu,
-                  double *gt, double *ut, double *st, double *score)
+                  double *gt, double *ut, double *st, double *score, int act)
 {
     const int ng = group > 0 ? d / group : 0;
 #pragma omp parallel for schedule(static)
@@ -275,7 +289,7 @@ void oracle_proxy(const uint16_t *x, int dtype, int B, int d, int f,
                 g += xi * wgt;
                 u += xi * wut;
             }
-            double s = silu(g) * u;
+            double s = oracle_gate_act(g, act) * u;
             if (gt)
                 gt[(size_t)b * f + j] = g;
             if (ut)
@@ -307,7 +321,7 @@ void oracle_select_channels(const double *score, int f, int k_ff, int32_t *ff_id
  */
 void oracle_stage2(const uint16_t *x, int dtype, int B, int d, int f,
                    const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
-                   const int32_t *ff_idx, int k_ff, double *s_out, double *y)
+                   const int32_t *ff_idx, int k_ff, double *s_out, double *y, int act)
 {
     (void)f;
     double *s = (double *)malloc(sizeof(double) * (size_t)B * (size_t)(k_ff > 0 ? k_ff : 1));
@@ -321,7 +335,7 @@ void oracle_stage2(const uint16_t *x, int dtype, int B, int d, int f,
                 g += xi * WV(wg, j, i);
                 u += xi * WV(wu, j, i);
             }
-            s[(size_t)b * k_ff + t] = silu(g) * u;
+            s[(size_t)b * k_ff + t] = oracle_gate_act(g, act) * u;
         }
     }
     const int cblk = 256;
@@ -350,7 +364,7 @@ void oracle_stage2(const uint16_t *x, int dtype, int B, int d, int f,
 /* ------------------------------------------------------------------ */
 void oracle_ffn_dense(const uint16_t *x, int dtype, int B, int d, int f,
                       const uint16_t *wg, const uint16_t *wu, const uint16_t *wd,
-                      double *y)
+                      double *y, int act)
 {
     double *s = (double *)malloc(sizeof(double) * (size_t)B * (size_t)f);
 #pragma omp parallel for schedule(static)
@@ -362,7 +376,7 @@ void oracle_ffn_dense(const uint16_t *x, int dtype, int B, int d, int f,
                 g += xi * WV(wg, j, i);
                 u += xi * WV(wu, j, i);
             }
-            s[(size_t)b * f + j] = u * silu(g);
+            s[(size_t)b * f + j] = u * oracle_gate_act(g, act);
         }
     }
     const int cblk = 256;
@@ -398,7 +412,7 @@ void oracle_ffn_sparse(const uint16_t *x, int dtype, int B, int d, int f,
                        const int8_t *cu, const uint16_t *su, int group,
                        int k_in, int k_ff, const int32_t *mask_override,
                        int32_t *in_idx_out, double *score_out, int32_t *ff_idx_out,
-                       double *y)
+                       double *y, int act)
 {
     int32_t *in_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)k_in);
     int32_t *ff_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)k_ff);
@@ -408,15 +422,15 @@ void oracle_ffn_sparse(const uint16_t *x, int dtype, int B, int d, int f,
         if (in_idx_out || score_out) {
             oracle_select_inputs(x, dtype, B, d, k_in, in_idx);
             oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
-                         wg, wu, NULL, NULL, NULL, score);
+                         wg, wu, NULL, NULL, NULL, score, act);
         }
     } else {
         oracle_select_inputs(x, dtype, B, d, k_in, in_idx);
         oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
-                     wg, wu, NULL, NULL, NULL, score);
+                     wg, wu, NULL, NULL, NULL, score, act);
         oracle_select_channels(score, f, k_ff, ff_idx);
     }
-    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y);
+    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y, act);
     if (in_idx_out)
         memcpy(in_idx_out, in_idx, sizeof(int32_t) * (size_t)k_in);
     if (score_out)
@@ -478,14 +492,14 @@ void oracle_ffn_sparse_tau(const uint16_t *x, int dtype, int B, int d, int f,
                            double tau_x, double tau_s,
                            const int32_t *mask_override, int n_override,
                            int32_t *in_idx_out, double *score_out, int32_t *ff_idx_out,
-                           int32_t *counts, double *y)
+                           int32_t *counts, double *y, int act)
 {
     int32_t *in_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)d);
     int32_t *ff_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)f);
     double *score = (double *)malloc(sizeof(double) * (size_t)f);
     int k_in = oracle_select_inputs_tau(x, dtype, B, d, tau_x, in_idx);
     oracle_proxy(x, dtype, B, d, f, in_idx, k_in, proxy_kind, cg, sg, cu, su, group,
-                 wg, wu, NULL, NULL, NULL, score);
+                 wg, wu, NULL, NULL, NULL, score, act);
     int k_ff;
     if (mask_override) {
         memcpy(ff_idx, mask_override, sizeof(int32_t) * (size_t)n_override);
@@ -493,7 +507,7 @@ void oracle_ffn_sparse_tau(const uint16_t *x, int dtype, int B, int d, int f,
     } else {
         k_ff = oracle_select_threshold(score, f, tau_s, ff_idx);
     }
-    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y);
+    oracle_stage2(x, dtype, B, d, f, wg, wu, wd, ff_idx, k_ff, NULL, y, act);
     if (in_idx_out)
         memcpy(in_idx_out, in_idx, sizeof(int32_t) * (size_t)k_in);
     if (score_out)

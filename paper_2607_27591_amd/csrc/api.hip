@@ -31,6 +31,7 @@ bool proxy_shape_ok(int d, int fmt, int group) {
 prox_status check_weights(const prox_weights *w) {
     if (!w || !w->w_gate || !w->w_up || !w->w_down) return PROX_ERR_INVALID;
     if (!dtype_ok(w->dtype)) return PROX_ERR_INVALID;
+    if (w->act != PROX_ACT_SILU && w->act != PROX_ACT_GELU) return PROX_ERR_INVALID;
     if (!aligned(w->w_gate, 16) || !aligned(w->w_up, 16) || !aligned(w->w_down, 16))
         return PROX_ERR_INVALID;
     if (w->d_model < 1 || w->d_ff < 1) return PROX_ERR_INVALID;
@@ -78,7 +79,8 @@ prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, i
         PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, w->w_gate, w->w_up, w->w_down,
                                scores, k_ff, mask, c0 == 0 ? scores_copy : nullptr,
                                W.ypart + (size_t)c0 * d, ystride, nwg,
-                               c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, stream));
+                               c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, w->act,
+                               stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
     PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));
@@ -129,7 +131,8 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
         const int nb = batch - c0 < pnb ? batch - c0 : pnb;
         const Select in_sel{rules.tau_mode, rules.tau_x, rules.counts};
         PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
-                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, stream));
+                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, w->act,
+                              stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[1], stream));
     const Select ff_sel{rules.tau_mode, rules.tau_s, rules.counts ? rules.counts + 1 : nullptr};

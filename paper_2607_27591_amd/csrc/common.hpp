@@ -77,6 +77,12 @@ __device__ __forceinline__ uint4 load_stream16(const void *p) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
+// Gate activation of the gated FFN: SiLU (act 0) or GELU z * Phi(z) (act 1),
+// with Phi(z) = erfc(-z / sqrt 2) / 2 (no cancellation in the negative tail).
+__device__ __forceinline__ float gate_act(float z, int act) {
+    return act == 0 ? silu(z) : 0.5f * z * erfcf(-z * 0.70710678118654752f);
+}
+
 // ---------------------------------------------------------------------------
 // Wave64 collectives
 // ---------------------------------------------------------------------------

@@ -21,9 +21,10 @@ hipError_t launch_unpack(int qbits, const void *blob, int d, int f, int group, i
 int proxy_max_nb(int d);
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,
-                        uint8_t *in_mask, float *scores, int accumulate, Select sel,
+                        uint8_t *in_mask, float *scores, int accumulate, Select sel, int act,
                         hipStream_t stream);
 
+// act (both stages): the gate activation, 0 SiLU or 1 GELU.
 // Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
 // the dense FFN over all f channels; otherwise the top k_ff scores, or the
 // threshold rule of sel, pick the channels.  Partial y rows go to
@@ -31,7 +32,7 @@ hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int 
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
                          uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, Select sel, hipStream_t stream);
+                         int nwg, Select sel, int act, hipStream_t stream);
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
                          hipStream_t stream);
 hipError_t launch_add_rmsnorm(int dtype, const void *x, const void *y, int batch, int d, float eps,

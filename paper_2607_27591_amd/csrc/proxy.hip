@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     int row0, int nb,                                 // rows [row0, row0 + nb) are projected
     int d, int f, int group, int k_in, const uint8_t *__restrict__ blob,
     uint8_t *__restrict__ in_mask, float *__restrict__ scores,
-    int accumulate, Select sel_rule) {   // k_in: the list capacity when sel_rule.tau_mode
+    int accumulate, Select sel_rule, int act) {   // k_in: the list capacity when sel_rule.tau_mode
     constexpr int CPL = proxy_cols<NB, QB>();
     constexpr int LPS = 2 * T / CPL;              // lanes per row segment (gate + up)
     constexpr int NGRP = kWave / LPS;             // lane groups per wave
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                             red[((2 * q + 1) * NB + b) * 2 * T + m2 * T + tid];
                 gu[m2] = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
             }
-            best = fmaxf(best, fabsf(silu(gu[0]) * gu[1]));
+            best = fmaxf(best, fabsf(gate_act(gu[0], act) * gu[1]));
         }
         if (j < f) scores[j] = accumulate ? fmaxf(scores[j], best) : best;
     }
@@ -435,7 +435,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
 template <int NB, int DT, int QB, int T, int C>
 static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                  int group, int k_in, const void *blob,
-                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
+                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
     const BlobLayout L(d, f, QB, group);
     const size_t lds = proxy_lds_bytes(k_in, d / group, NB, T);
     if (lds > 65536) {
@@ -446,7 +446,7 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
     }
     proxy_kernel<NB, DT, QB, T, C><<<L.n_tiles, kBlock, lds, s>>>(
         static_cast<const uint16_t *>(x_all), B_all, row0, nb, d, f, group, k_in,
-        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel_rule);
+        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel_rule, act);
     return hipGetLastError();
 }
 
@@ -454,39 +454,39 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
 template <int NB, int DT, int QB, int T>
 static hipError_t launch_proxy_c(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                  int group, int k_in, const void *blob,
-                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
+                                 uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
     if (d <= 8 * kBlock)
-        return launch_proxy_t<NB, DT, QB, T, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-    return launch_proxy_t<NB, DT, QB, T, 16>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+        return launch_proxy_t<NB, DT, QB, T, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
+    return launch_proxy_t<NB, DT, QB, T, 16>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
 }
 
 template <int DT, int QB, int T>
 static hipError_t launch_proxy_nb(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                   int group, int k_in, const void *blob,
-                                  uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
+                                  uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
     switch (proxy_nb_t(nb)) {
-        case 1: return launch_proxy_c<1, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-        case 2: return launch_proxy_c<2, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-        default: return launch_proxy_c<4, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+        case 1: return launch_proxy_c<1, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
+        case 2: return launch_proxy_c<2, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
+        default: return launch_proxy_c<4, DT, QB, T>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
     }
 }
 
 template <int DT, int QB>
 static hipError_t launch_proxy_tile(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                     int group, int k_in, const void *blob,
-                                    uint8_t *in_mask, float *scores, int accumulate, Select sel_rule,
+                                    uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act,
                                     hipStream_t s) {
     if (proxy_tile(f) == 128)
-        return launch_proxy_nb<DT, QB, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
-    return launch_proxy_nb<DT, QB, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s);
+        return launch_proxy_nb<DT, QB, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
+    return launch_proxy_nb<DT, QB, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
 }
 
 int proxy_max_nb(int d) { return d <= 8192 ? kProxyMaxNB : 2; }
 
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,
-                        uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, hipStream_t s) {
-#define PX(DT_, QB_) launch_proxy_tile<DT_, QB_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, s)
+                        uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
+#define PX(DT_, QB_) launch_proxy_tile<DT_, QB_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s)
     if (dtype == kBF16) return qbits == 4 ? PX(kBF16, 4) : qbits == 8 ? PX(kBF16, 8) : PX(kBF16, 16);
     return qbits == 4 ? PX(kF16, 4) : qbits == 8 ? PX(kF16, 8) : PX(kF16, 16);
 #undef PX

@@ -62,7 +62,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const float *__restrict__ scores,   // NULL: dense FFN over all f channels
     int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
     float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
-    Select sel_rule) {
+    Select sel_rule, int act) {                     // act: gate activation
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
             const float us = wave_sum(au[b]);
             if (lane == 0) {
                 if (Q == 1) {
-                    s_sh[t * NB + b] = silu(gs) * us;
+                    s_sh[t * NB + b] = gate_act(gs, act) * us;
                 } else {
                     sm.gu[((t * Q + q) * 2 + b) * 2 + 0] = gs;
                     sm.gu[((t * Q + q) * 2 + b) * 2 + 1] = us;
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                 gs += sm.gu[((t * Q + q) * 2 + b) * 2 + 0];
                 us += sm.gu[((t * Q + q) * 2 + b) * 2 + 1];
             }
-            s_sh[t * NB + b] = silu(gs) * us;
+            s_sh[t * NB + b] = gate_act(gs, act) * us;
         }
         __syncthreads();
     }
@@ -372,14 +372,14 @@ template <int NB, int DT, int C>
 static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
                                   uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, Select sel_rule, hipStream_t st) {
+                                  int ystride, int nwg, Select sel_rule, int act, hipStream_t st) {
     const size_t lds = stage2_lds_bytes(d, NB);
     hipError_t e = allow_lds(stage2_kernel<NB, DT, C>, lds);
     if (e != hipSuccess) return e;
     stage2_kernel<NB, DT, C><<<nwg, kBlock, lds, st>>>(
         static_cast<const uint16_t *>(x), nb, d, f, static_cast<const uint16_t *>(wg),
         static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff,
-        mask, scores_copy, ypart, ystride, sel_rule);
+        mask, scores_copy, ypart, ystride, sel_rule, act);
     return hipGetLastError();
 }
 
@@ -387,28 +387,28 @@ template <int NB, int DT>
 static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const void *wg,
                                   const void *wu, const void *wd, const float *scores, int k_ff,
                                   uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, Select sel_rule, hipStream_t st) {
+                                  int ystride, int nwg, Select sel_rule, int act, hipStream_t st) {
     // C = score rows per thread of the channel top-k (the dense path has none).
     if (!scores || f <= 16 * kBlock)
         return launch_stage2_t<NB, DT, 16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, sel_rule, st);
+                                           scores_copy, ypart, ystride, nwg, sel_rule, act, st);
     if (f <= 32 * kBlock)
         return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, sel_rule, st);
+                                           scores_copy, ypart, ystride, nwg, sel_rule, act, st);
     return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                       scores_copy, ypart, ystride, nwg, sel_rule, st);
+                                       scores_copy, ypart, ystride, nwg, sel_rule, act, st);
 }
 
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
                          const void *wu, const void *wd, const float *scores, int k_ff,
                          uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, Select sel_rule, hipStream_t st) {
+                         int nwg, Select sel_rule, int act, hipStream_t st) {
 #define S2(NB_)                                                                                    \
     return dtype == kBF16                                                                          \
                ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,    \
-                                             scores_copy, ypart, ystride, nwg, sel_rule, st)                 \
+                                             scores_copy, ypart, ystride, nwg, sel_rule, act, st)                 \
                : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,     \
-                                            scores_copy, ypart, ystride, nwg, sel_rule, st)
+                                            scores_copy, ypart, ystride, nwg, sel_rule, act, st)
     switch (stage2_nb_t(nb)) {
         case 1: S2(1);
         case 2: S2(2);

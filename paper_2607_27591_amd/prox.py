@@ -36,7 +36,10 @@ class ProxError(RuntimeError):
 class _Weights(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int), ("d_ff", ctypes.c_int), ("dtype", ctypes.c_int),
                 ("w_gate", ctypes.c_void_p), ("w_up", ctypes.c_void_p),
-                ("w_down", ctypes.c_void_p)]
+                ("w_down", ctypes.c_void_p), ("act", ctypes.c_int)]
+
+
+SILU, GELU = 0, 1   # gate activations: SwiGLU, GeGLU
 
 
 class _Proxy(ctypes.Structure):
@@ -119,10 +122,12 @@ def _dev_tensor(t: torch.Tensor, what: str, dtype=None) -> torch.Tensor:
 
 @dataclasses.dataclass
 class Weights:
-    """Channel-major SwiGLU weights, each [d_ff][d_model] in fp16 or bf16."""
+    """Channel-major gated-FFN weights, each [d_ff][d_model] in fp16 or bf16;
+    act is the gate activation (SILU: SwiGLU, GELU: GeGLU)."""
     w_gate: torch.Tensor
     w_up: torch.Tensor
     w_down: torch.Tensor
+    act: int = SILU
 
     @property
     def d_ff(self) -> int:
@@ -145,7 +150,7 @@ class Weights:
             if tuple(t.shape) != (self.d_ff, self.d_model):
                 raise ValueError(f"{name} must be [d_ff][d_model]")
         return _Weights(self.d_model, self.d_ff, dt, self.w_gate.data_ptr(),
-                        self.w_up.data_ptr(), self.w_down.data_ptr())
+                        self.w_up.data_ptr(), self.w_down.data_ptr(), int(self.act))
 
 
 @dataclasses.dataclass

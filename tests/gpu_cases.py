@@ -44,16 +44,18 @@ class Case:
     scales_g: np.ndarray
     codes_u: np.ndarray
     scales_u: np.ndarray
+    act: int = prox.SILU
 
 
-def make_case(cfg: W.FFNConfig, device="cuda") -> Case:
+def make_case(cfg: W.FFNConfig, device="cuda", act: int = prox.SILU) -> Case:
     wl = W.make_workload(cfg)
-    w = prox.Weights(*(prox.from_bits(m, cfg.dtype, device) for m in (wl.w_gate, wl.w_up, wl.w_down)))
+    w = prox.Weights(*(prox.from_bits(m, cfg.dtype, device) for m in (wl.w_gate, wl.w_up, wl.w_down)),
+                     act=act)
     fmt = prox.INT4 if cfg.qbits == 4 else prox.INT8
     p = prox.pack_proxy(w, fmt, cfg.group)
     cg, sg = oracle.quantize(wl.w_gate, cfg.dtype, cfg.qbits, cfg.group)
     cu, su = oracle.quantize(wl.w_up, cfg.dtype, cfg.qbits, cfg.group)
-    return Case(cfg, wl, w, p, cg, sg, cu, su)
+    return Case(cfg, wl, w, p, cg, sg, cu, su, act)
 
 
 def check_pack(case: Case) -> None:
@@ -103,7 +105,8 @@ def check_sparse(case: Case, x_bits: np.ndarray, k_in: int, k_ff: int, out: GpuO
     x_bits = np.atleast_2d(x_bits)
     ref = oracle.ffn_sparse(x_bits, cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down,
                             k_in, k_ff, codes_g=case.codes_g, scales_g=case.scales_g,
-                            codes_u=case.codes_u, scales_u=case.scales_u, group=cfg.group)
+                            codes_u=case.codes_u, scales_u=case.scales_u, group=cfg.group,
+                            act=case.act)
     # (a) input top-k, bit-exact
     assert np.array_equal(np.flatnonzero(out.in_mask), ref["in_idx"]), f"{tag}: input top-k"
     # (b) channel selection is the exact top-k of the GPU's own scores
@@ -126,7 +129,7 @@ def check_sparse(case: Case, x_bits: np.ndarray, k_in: int, k_ff: int, out: GpuO
     # (e) y against the oracle on the GPU's mask
     gpu_ff = np.flatnonzero(out.mask).astype(np.int32)
     _, y_ref = oracle.stage2(x_bits, cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down,
-                             gpu_ff)
+                             gpu_ff, act=case.act)
     yerr = y_rel_err(out.y, y_ref, cfg.dtype)
     assert yerr <= Y_TOL, f"{tag}: y max-abs-rel {yerr}"
     return {"score_err_rel": serr / max(smax, 1e-30), "mask_agree": agree,

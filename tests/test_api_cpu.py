@@ -50,8 +50,8 @@ def test_library_is_gfx950_only():
         assert f"amdgcn-amd-amdhsa--{other}" not in out
 
 
-def _weights(d=1024, f=3072, dtype=prox.BF16, g=FAKE, u=FAKE, dn=FAKE):
-    return prox._Weights(d, f, dtype, g, u, dn)
+def _weights(d=1024, f=3072, dtype=prox.BF16, g=FAKE, u=FAKE, dn=FAKE, act=prox.SILU):
+    return prox._Weights(d, f, dtype, g, u, dn, act)
 
 
 def _proxy(fmt=prox.INT4, group=128, blob=FAKE, nbytes=1 << 40):

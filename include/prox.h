@@ -124,6 +124,17 @@ prox_status prox_unpack_proxy(const prox_proxy *p, int d_model, int d_ff, int8_t
 size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
 
 /*
+ * Which Stage-1 kernel a sparse call takes (for inspection and tests): the
+ * batch rows one launch of the matrix-core kernel covers for this shape, or 0
+ * when Stage 1 runs on the dot-product kernel (an INT8 or unquantised proxy,
+ * fewer than five batch rows, or a kept-input list too long for the LDS, or
+ * an unsupported shape).  k_in is the kept-input count; the threshold entry
+ * point sizes its list for k_in = d_model.  Host only, no HIP calls.  The two
+ * kernels compute the same proxy in a different fp32 summation order.
+ */
+int prox_stage1_mfma_rows(int d_model, prox_qfmt fmt, int group, int batch, int k_in);
+
+/*
  * Dense SwiGLU FFN (Sec. 2.1):  y = (x W_up (.) SiLU(x W_gate)) W_down.
  *   x: device [batch][d_model], w->dtype;  y: device [batch][d_model], same
  *   dtype, rounded once (round-to-nearest-even) from fp32 accumulation.

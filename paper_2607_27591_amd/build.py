@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libprox.so")
-SOURCES = ["api.hip", "calib.hip", "pack.hip", "proxy.hip", "stage2.hip"]
+SOURCES = ["api.hip", "calib.hip", "pack.hip", "proxy.hip", "proxy_mfma.hip", "stage2.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

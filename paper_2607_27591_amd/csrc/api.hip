@@ -88,6 +88,11 @@ prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, i
     return PROX_OK;
 }
 
+// Batch rows per matrix-core Stage-1 launch, or 0 for the dot-product kernel.
+int stage1_mfma_rows(int d, int qbits, int group, int batch, int k_in) {
+    return qbits == 4 && batch >= kProxyMfmaMinRows ? proxy_mfma_rows(d, group, k_in) : 0;
+}
+
 // The selection of each stage: counts (k_in, k_ff) or thresholds.
 struct Rules {
     int tau_mode;
@@ -126,13 +131,21 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
     const Ws W = carve(ws, d, f, batch);
     const int dt = w->dtype;
     if (events) PROX_TRY(hipEventRecord(events[0], stream));
-    const int pnb = proxy_max_nb(d);
+    // Several batch rows with an INT4 proxy: the matrix-core kernel, which
+    // reads the codes once for up to 16 rows; else the dot-product kernel.
+    const int mfma_rows = stage1_mfma_rows(d, qbits, p->group, batch, k_in);
+    const int pnb = mfma_rows ? mfma_rows : proxy_max_nb(d);
     for (int c0 = 0; c0 < batch; c0 += pnb) {
         const int nb = batch - c0 < pnb ? batch - c0 : pnb;
         const Select in_sel{rules.tau_mode, rules.tau_x, rules.counts};
-        PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
-                              c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, w->act,
-                              stream));
+        if (mfma_rows)
+            PROX_TRY(launch_proxy_mfma(dt, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
+                                       c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel,
+                                       w->act, stream));
+        else
+            PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
+                                  c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, w->act,
+                                  stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[1], stream));
     const Select ff_sel{rules.tau_mode, rules.tau_s, rules.counts ? rules.counts + 1 : nullptr};
@@ -157,6 +170,13 @@ const char *prox_strerror(prox_status s) {
 
 const char *prox_sparse_stage_name(int i) {
     return i >= 0 && i < PROX_SPARSE_STAGES ? kStageNames[i] : nullptr;
+}
+
+int prox_stage1_mfma_rows(int d_model, prox_qfmt fmt, int group, int batch, int k_in) {
+    if (d_model < 1 || d_model > kMaxDModel || !proxy_shape_ok(d_model, fmt, group) ||
+        batch < 1 || batch > PROX_MAX_BATCH || k_in < 1 || k_in > d_model)
+        return 0;
+    return stage1_mfma_rows(d_model, qbits_of(fmt), group, batch, k_in);
 }
 
 size_t prox_proxy_bytes(int d_model, int d_ff, prox_qfmt fmt, int group) {

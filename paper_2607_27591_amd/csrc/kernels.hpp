@@ -24,6 +24,16 @@ hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int 
                         uint8_t *in_mask, float *scores, int accumulate, Select sel, int act,
                         hipStream_t stream);
 
+// Stage 1 on the matrix cores for INT4 proxies: batch rows [row0, row0 + nb)
+// with nb <= proxy_mfma_rows(d, group, k_in) (16, 8, or 0 when the kept-row
+// list does not fit in LDS); otherwise as launch_proxy.
+int proxy_mfma_rows(int d, int group, int k_in);
+hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, int nb, int d,
+                             int f, int group, int k_in, const void *blob, uint8_t *in_mask,
+                             float *scores, int accumulate, Select sel, int act,
+                             hipStream_t stream);
+constexpr int kProxyMfmaMinRows = 5;   // batch rows from which Stage 1 uses the matrix cores
+
 // act (both stages): the gate activation, 0 SiLU or 1 GELU.
 // Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
 // the dense FFN over all f channels; otherwise the top k_ff scores, or the

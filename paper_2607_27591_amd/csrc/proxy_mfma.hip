@@ -1,0 +1,354 @@
+// Stage 1 of the sparse decode step for several batch rows at once, on the
+// matrix cores (Sec. 4.1 Stage 1 with the INT4 proxy of Sec. 3.2 / 4.3).  It
+// computes what proxy_kernel computes (the same input selection, the same
+// per-group scales and the same score) for up to 16 rows per launch, so the
+// proxy codes of a kept input row are read once for all of them.
+//
+// The proxy GEMV of a column tile is a product of x (batch rows x kept input
+// rows) with the dequantised codes (kept input rows x columns), done as
+// 16 x 16 x 16 MFMAs (bf16 or fp16 operands, fp32 accumulation).  The kept-row
+// list is padded per quantisation group to a multiple of 16, so one 16-row
+// block never mixes groups.  A pad row repeats a kept row of its group (its
+// codes come from lines that are read anyway) and has x = 0.
+//
+// Lane l of a wave feeds batch row l % 16 to the A operand and column set
+// l % 16 to the B operand, for block rows 4 (l / 16) .. 4 (l / 16) + 3.  In a
+// 64-column half of the tile and one matrix (gate or up, per wave) the lane
+// owns columns 4n .. 4n + 3 (n = l % 16).  Per block it loads 2 bytes (4
+// codes) from each of its 4 rows, pairs the rows, and ORs each nibble under
+// the exponent of the magic constant M.  That gives the exact 16-bit pair
+// (M + n_a, M + n_b), n = q + 8, and two such pairs are one B operand: 4 MFMAs
+// per block.  Waves split the blocks of their half and matrix, so a wave may
+// see only part of a group: a fifth MFMA per block, with B all ones, sums x
+// over the blocks the wave has taken, in the accumulator layout, and at a
+// group change the lane subtracts (M + 8) times that sum and applies the
+// group's scale.  The waves' partial sums meet in LDS in wave order, so results are
+// deterministic.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "topk.hpp"
+
+namespace prox {
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned short us2 __attribute__((ext_vector_type(2)));   // two rows' codes, one VGPR
+
+constexpr int kMfmaBlock = 16;    // kept input rows per block (the MFMA's K)
+constexpr int kMfmaU = 4;         // blocks in flight per wave
+
+template <int DT>
+struct MfmaMagic;
+template <>
+struct MfmaMagic<kBF16> {   // 128.0 in bf16; 128 + n is exact for n < 128
+    static constexpr uint32_t pair = 0x43004300u;
+    static constexpr uint32_t ones = 0x3F803F80u;   // (1.0, 1.0)
+    static constexpr float offset = 136.0f;   // M + 8 (the code bias)
+};
+template <>
+struct MfmaMagic<kF16> {    // 1024.0 in fp16; 1024 + n is exact for n < 1024
+    static constexpr uint32_t pair = 0x64006400u;
+    static constexpr uint32_t ones = 0x3C003C00u;
+    static constexpr float offset = 1032.0f;
+};
+
+template <int DT>
+__device__ __forceinline__ v4f mfma16(uint2 a, uint2 b, v4f c) {
+    if constexpr (DT == kBF16)
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(v4s, a),
+                                                         __builtin_bit_cast(v4s, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a),
+                                                     __builtin_bit_cast(v4h, b), c, 0, 0, 0);
+}
+
+// Dynamic LDS: rows [cap] u16, x [NX][cap] u16, block groups [cap / 16] u16;
+// after the stream the same space holds the cross-wave partial sums
+// [16 waves][64 lanes][16] f32.
+__host__ __device__ inline int mfma_list_cap(int k_in, int ng) {
+    return (k_in + ng * (kMfmaBlock - 1) + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
+}
+__host__ __device__ inline size_t mfma_list_bytes(int cap, int nx) {
+    return align_up((size_t)cap * 2, 16) + align_up((size_t)nx * cap * 2, 16) +
+           align_up((size_t)(cap / kMfmaBlock) * 2, 16);
+}
+constexpr size_t kMfmaRedBytes = (size_t)kMaxBlockWaves * kWave * 16 * 4;   // 64 KiB
+__host__ __device__ inline size_t mfma_lds_bytes(int k_in, int ng, int nx) {
+    const size_t list = mfma_list_bytes(mfma_list_cap(k_in, ng), nx);
+    return list > kMfmaRedBytes ? list : kMfmaRedBytes;
+}
+
+template <int DT, int T, int C, int NX>
+__global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
+    const uint16_t *__restrict__ x_all, int B_all, int row0, int nb, int d, int f, int group,
+    int k_in, const uint8_t *__restrict__ blob, uint8_t *__restrict__ in_mask,
+    float *__restrict__ scores, int accumulate, Select sel_rule, int act) {
+    static_assert(T == 64 || T == 128, "tile widths of the blob layout");
+    static_assert(NX == 8 || NX == 16, "x rows kept in LDS");
+    constexpr int WH = T / 64;                       // 64-column halves per tile
+    constexpr int WPG = kMaxBlockWaves / (WH * 2);   // waves per (half, matrix)
+    constexpr uint32_t M = MfmaMagic<DT>::pair;
+    constexpr float off = MfmaMagic<DT>::offset;
+    const BlobLayout L(d, f, 4, group);
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+    const int tile = blockIdx.x;
+    const int ng = d / group;
+
+    __shared__ TopKScratch tk;
+    __shared__ TopKOrder<C> ord;
+    __shared__ int gsel0[kMaxDModel / 128 + 1];   // kept rows before each group
+    __shared__ int gstart[kMaxDModel / 128 + 1];  // padded list position of each group
+    extern __shared__ __align__(16) unsigned char dsm[];
+
+    const int cap = mfma_list_cap(k_in, ng);
+    uint16_t *rows_sh = reinterpret_cast<uint16_t *>(dsm);
+    uint16_t *xs_sh = reinterpret_cast<uint16_t *>(dsm + align_up((size_t)cap * 2, 16));
+    uint16_t *kbg_sh = reinterpret_cast<uint16_t *>(dsm + align_up((size_t)cap * 2, 16) +
+                                                    align_up((size_t)NX * cap * 2, 16));
+
+    // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
+    uint32_t key[C];
+#pragma unroll
+    for (int r = 0; r < C; ++r) key[r] = 0u;
+    for (int b = 0; b < B_all; ++b) {
+        const uint16_t *xb = x_all + (size_t)b * d;
+        uint32_t raw[C];
+#pragma unroll
+        for (int r = 0; r < C; ++r) raw[r] = xb[min(r * kBlock + tid, d - 1)];
+#pragma unroll
+        for (int r = 0; r < C; ++r)
+            if (r * kBlock + tid < d) key[r] = max(key[r], raw[r] & 0x7FFFu);
+    }
+    uint64_t sel = 0;
+    if (sel_rule.tau_mode) {
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
+            sel |= (uint64_t)in << r;
+        }
+        topk_order<kBlock, C>(sel, d, tk, ord);
+        if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
+            *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
+    } else {
+        sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+    }
+
+    // ---- groups: kept rows per group, list starts padded to whole blocks ----
+    for (int g = tid; g <= ng; g += kBlock) gsel0[g] = topk_selected_before<kBlock, C>(ord, g * group);
+    __syncthreads();
+    if (wid == 0) {
+        int carry = 0;
+        for (int g0 = 0; g0 <= ng; g0 += kWave) {
+            const int g = g0 + lane;
+            const int cnt = g < ng ? gsel0[g + 1] - gsel0[g] : 0;
+            const int padded = (cnt + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
+            const int incl = wave_inclusive_scan(padded);
+            if (g <= ng) gstart[g] = carry + incl - padded;
+            carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+    }
+    __syncthreads();
+
+    // ---- kept rows and their x values to the list ----
+    const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;   // i / group, exact here
+    auto list_pos = [&](int r) {
+        const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
+        return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
+    };
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        const int i = r * kBlock + tid;
+        if (i >= d) continue;
+        const bool s = (sel >> r) & 1;
+        if (tile == 0 && in_mask) in_mask[i] = s ? 1 : 0;
+        if (s) rows_sh[list_pos(r)] = (uint16_t)i;
+    }
+    for (int b = 0; b < NX; ++b) {
+        const uint16_t *xb = x_all + (size_t)(row0 + min(b, nb - 1)) * d;
+#pragma unroll
+        for (int r = 0; r < C; ++r) {
+            const int i = r * kBlock + tid;
+            const uint16_t xv = xb[min(i, d - 1)];
+            if (i < d && ((sel >> r) & 1)) xs_sh[b * cap + list_pos(r)] = b < nb ? xv : (uint16_t)0;
+        }
+    }
+    __syncthreads();   // the kept rows are in place: pads copy the group's last one
+    for (int g = tid; g < ng; g += kBlock) {
+        const int cnt = gsel0[g + 1] - gsel0[g];
+        const int p0 = gstart[g], p1 = gstart[g + 1];
+        for (int p = p0 + cnt; p < p1; ++p) {   // p1 > p0 + cnt only when cnt > 0
+            rows_sh[p] = rows_sh[p0 + cnt - 1];
+            for (int b = 0; b < NX; ++b) xs_sh[b * cap + p] = 0;
+        }
+        for (int kb = p0 / kMfmaBlock; kb < p1 / kMfmaBlock; ++kb) kbg_sh[kb] = (uint16_t)g;
+    }
+    __syncthreads();
+
+    // ---- stream the blocks: this wave's half and share of the blocks ----
+    const int nkb = gstart[ng] / kMfmaBlock;
+    const int hm = wid / WPG, wi = wid % WPG;
+    const int h = hm / 2, mat = hm % 2;             // column half, matrix (0 gate, 1 up)
+    const int kb0 = (int)((long long)wi * nkb / WPG), kb1 = (int)((long long)(wi + 1) * nkb / WPG);
+    const int ln = lane % 16, lg = lane / 16;
+    const uint8_t *tbase = blob + L.codes_offset + (size_t)tile * L.row_bytes + mat * (T / 2) +
+                           h * 32 + ln * 2;
+    const uint16_t *sbase = reinterpret_cast<const uint16_t *>(blob + L.scales_offset) +
+                            (size_t)tile * ng * 2 * T + (size_t)mat * T + h * 64 + ln * 4;
+    const uint32_t rstride = (uint32_t)L.row_stride;
+
+    v4f acc[4], tot[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        acc[c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        tot[c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    v4f xacc = v4f{0.0f, 0.0f, 0.0f, 0.0f};   // x sums of this wave's blocks, current group
+    const uint2 ones = make_uint2(MfmaMagic<DT>::ones, MfmaMagic<DT>::ones);
+
+    if (kb0 < kb1) {
+        int gcur = kbg_sh[kb0];
+        // this lane's 4 fp16 scales of the current group
+        uint2 sc = *reinterpret_cast<const uint2 *>(sbase + (size_t)gcur * 2 * T);
+        auto flush = [&]() {
+            const uint32_t sw[2] = {sc.x, sc.y};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float s = f16_bits_to_float((c & 1) ? (sw[c >> 1] >> 16) : (sw[c >> 1] & 0xFFFFu));
+#pragma unroll
+                for (int j = 0; j < 4; ++j) tot[c][j] = fmaf(s, acc[c][j] - off * xacc[j], tot[c][j]);
+                acc[c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+            xacc = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        };
+        for (int kb = kb0; kb < kb1; kb += kMfmaU) {
+            // All loads first (the tail repeats the last block, unused).
+            us2 code[kMfmaU][2];   // [block]: rows (0, 1) and (2, 3)
+            uint2 xa[kMfmaU];
+            int gk[kMfmaU];
+#pragma unroll
+            for (int u = 0; u < kMfmaU; ++u) {
+                const int k = min(kb + u, kb1 - 1);
+                const uint2 rr = *reinterpret_cast<const uint2 *>(rows_sh + k * kMfmaBlock + lg * 4);
+                const uint32_t r4[4] = {rr.x & 0xFFFFu, rr.x >> 16, rr.y & 0xFFFFu, rr.y >> 16};
+                xa[u] = ln < NX ? *reinterpret_cast<const uint2 *>(xs_sh + ln * cap + k * kMfmaBlock + lg * 4)
+                                : make_uint2(0u, 0u);
+                gk[u] = kbg_sh[k];
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    code[u][q].x = *reinterpret_cast<const uint16_t *>(tbase + r4[2 * q] * rstride);
+                    code[u][q].y = *reinterpret_cast<const uint16_t *>(tbase + r4[2 * q + 1] * rstride);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kMfmaU; ++u) {
+                if (kb + u >= kb1) break;   // uniform
+                if (gk[u] != gcur) {
+                    flush();
+                    gcur = gk[u];
+                    sc = *reinterpret_cast<const uint2 *>(sbase + (size_t)gcur * 2 * T);
+                }
+                xacc = mfma16<DT>(xa[u], ones, xacc);   // x sums of rows 4 lg + j
+                const uint32_t p01 = __builtin_bit_cast(uint32_t, code[u][0]);   // rows a, b
+                const uint32_t p23 = __builtin_bit_cast(uint32_t, code[u][1]);   // rows c, d
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint2 bop = make_uint2(((p01 >> (4 * c)) & 0x000F000Fu) | M,
+                                                 ((p23 >> (4 * c)) & 0x000F000Fu) | M);
+                    acc[c] = mfma16<DT>(xa[u], bop, acc[c]);
+                }
+            }
+        }
+        flush();
+    }
+
+    // ---- partial sums of the waves meet in LDS, in wave order ----
+    __syncthreads();   // the list is dead
+    float *red = reinterpret_cast<float *>(dsm);   // [wave][lane][c * 4 + j]
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        *reinterpret_cast<float4 *>(red + ((size_t)(wid * kWave + lane) * 16 + c * 4)) =
+            make_float4(tot[c][0], tot[c][1], tot[c][2], tot[c][3]);
+    __syncthreads();
+    // Output o = ((m * 16 + b) * T + col): thread t sums outputs t, t + kBlock, ...
+    constexpr int NOUT = 2 * 16 * T;
+    constexpr int PER = NOUT / kBlock;
+    float outv[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const int o = tid + q * kBlock;
+        const int m = o / (16 * T), b = (o / T) % 16, col = o % T;
+        const int hh = col / 64, cl = col % 64;
+        const int src_lane = (b / 4) * 16 + cl / 4, c = cl % 4, j = b % 4;
+        const int wbase = (hh * 2 + m) * WPG;   // the waves of this (half, matrix)
+        float s = 0.0f;
+        for (int w2 = 0; w2 < WPG; ++w2)
+            s += red[(size_t)((wbase + w2) * kWave + src_lane) * 16 + c * 4 + j];
+        outv[q] = s;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q) red[tid + q * kBlock] = outv[q];
+    __syncthreads();
+    if (tid < T) {
+        const int j = tile * T + tid;
+        float best = 0.0f;
+        for (int b = 0; b < nb; ++b) {
+            const float gv = red[(0 * 16 + b) * T + tid], uv = red[(1 * 16 + b) * T + tid];
+            best = fmaxf(best, fabsf(gate_act(gv, act) * uv));
+        }
+        if (j < f) scores[j] = accumulate ? fmaxf(scores[j], best) : best;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launcher
+// ---------------------------------------------------------------------------
+
+int proxy_mfma_rows(int d, int group, int k_in) {
+    const int ng = d / group;
+    const size_t limit = 136 * 1024;   // dynamic LDS beside the ~22 KiB of statics
+    if (mfma_lds_bytes(k_in, ng, 16) <= limit) return 16;
+    if (mfma_lds_bytes(k_in, ng, 8) <= limit) return 8;
+    return 0;
+}
+
+template <int DT, int T, int C, int NX>
+static hipError_t launch_mfma_t(const void *x_all, int B_all, int row0, int nb, int d, int f,
+                                int group, int k_in, const void *blob, uint8_t *in_mask,
+                                float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+    const BlobLayout L(d, f, 4, group);
+    const size_t lds = mfma_lds_bytes(k_in, d / group, NX);
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void *>(proxy_mfma_kernel<DT, T, C, NX>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    proxy_mfma_kernel<DT, T, C, NX><<<L.n_tiles, kBlock, lds, s>>>(
+        static_cast<const uint16_t *>(x_all), B_all, row0, nb, d, f, group, k_in,
+        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel, act);
+    return hipGetLastError();
+}
+
+template <int DT, int T>
+static hipError_t launch_mfma_c(const void *x_all, int B_all, int row0, int nb, int d, int f,
+                                int group, int k_in, const void *blob, uint8_t *in_mask,
+                                float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+    const int nx = proxy_mfma_rows(d, group, k_in);
+#define MF(C_, NX_) launch_mfma_t<DT, T, C_, NX_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
+    if (d <= 8 * kBlock) return nx == 16 ? MF(8, 16) : MF(8, 8);
+    return nx == 16 ? MF(16, 16) : MF(16, 8);
+#undef MF
+}
+
+hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, int nb, int d,
+                             int f, int group, int k_in, const void *blob, uint8_t *in_mask,
+                             float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+    if (nb < 1 || nb > proxy_mfma_rows(d, group, k_in)) return hipErrorInvalidValue;
+    if (proxy_tile(f) == 128)
+        return dtype == kBF16 ? launch_mfma_c<kBF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
+                              : launch_mfma_c<kF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s);
+    return dtype == kBF16 ? launch_mfma_c<kBF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
+                          : launch_mfma_c<kF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s);
+}
+
+}  // namespace prox

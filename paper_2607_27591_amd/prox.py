@@ -66,6 +66,8 @@ def lib() -> ctypes.CDLL:
         L.prox_unpack_proxy.argtypes = [PP, I, I, P, P, P, P, P]
         L.prox_workspace_bytes.argtypes = [I, I, I]
         L.prox_workspace_bytes.restype = S
+        L.prox_stage1_mfma_rows.argtypes = [I, I, I, I, I]
+        L.prox_stage1_mfma_rows.restype = I
         L.prox_ffn_dense.argtypes = [WP, P, I, P, P, S, P]
         L.prox_ffn_sparse.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P]
         L.prox_ffn_sparse_staged.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
@@ -167,6 +169,12 @@ class Proxy:
 
 def proxy_bytes(d_model: int, d_ff: int, fmt: int, group: int) -> int:
     return int(lib().prox_proxy_bytes(d_model, d_ff, fmt, group))
+
+
+def stage1_mfma_rows(d_model: int, fmt: int, group: int, batch: int, k_in: int) -> int:
+    """Batch rows per matrix-core Stage-1 launch, 0 when the dot-product
+    kernel runs (threshold mode: pass k_in = d_model)."""
+    return int(lib().prox_stage1_mfma_rows(d_model, fmt, group, batch, k_in))
 
 
 def workspace_bytes(d_model: int, d_ff: int, batch: int) -> int:

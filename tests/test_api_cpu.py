@@ -82,6 +82,27 @@ def test_sizes():
     assert prox.workspace_bytes(4096, 12288, 16) > prox.workspace_bytes(4096, 12288, 1)
 
 
+def test_stage1_kernel_selection():
+    # The matrix-core Stage 1 takes INT4 proxies from five batch rows on, with
+    # 16 rows per launch while the kept-row list and 16 x rows fit the LDS,
+    # then 8; otherwise (and for INT8, unquantised or bad shapes) the
+    # dot-product kernel (0).
+    rows = prox.stage1_mfma_rows
+    assert rows(4096, prox.INT4, 128, 16, 2048) == 16
+    assert rows(4096, prox.INT4, 128, 5, 2048) == 16
+    assert rows(4096, prox.INT4, 128, 4, 2048) == 0        # four rows: dot product
+    assert rows(4096, prox.INT4, 128, 12, 4096) == 8       # threshold-mode list
+    assert rows(8192, prox.INT4, 128, 16, 3277) == 8
+    assert rows(8192, prox.INT4, 128, 16, 8192) == 0       # list too long
+    assert rows(16384, prox.INT4, 128, 6, 4915) == 8
+    assert rows(4096, prox.INT8, 128, 16, 2048) == 0
+    assert rows(4096, prox.NONE, 4096, 16, 2048) == 0
+    assert rows(4096, prox.INT4, 96, 16, 2048) == 0        # group % 128
+    assert rows(4096, prox.INT4, 128, 17, 2048) == 0       # batch
+    assert rows(4096, prox.INT4, 128, 16, 0) == 0          # k_in
+    assert rows(4096, prox.INT4, 128, 16, 4097) == 0
+
+
 def test_sparse_rejects_bad_arguments():
     L = prox.lib()
     assert _sparse(k_in=0) == INVALID

@@ -28,6 +28,16 @@ SMALL = {
     "bf16_i8_g128_640x513_b3": W.small_config(d=640, f=513, batch=3, seed=8, qbits=8),
     "bf16_i4_2048x3000_b4": W.small_config(d=2048, f=3000, batch=4, seed=9, in_frac=0.4,
                                            sigma_w=0.02),
+    # Five or more rows run on the matrix-core proxy: fp16 codes, and a 4096-wide
+    # input whose threshold-mode list allows only 8 rows per launch (two
+    # launches, the second accumulating into the scores).
+    "f16_i4_768x900_b7": W.small_config(d=768, f=900, batch=7, seed=13, dtype=W.DT_F16),
+    "bf16_i4_4096x1500_b12": W.small_config(d=4096, f=1500, batch=12, seed=14, in_frac=0.7,
+                                            sigma_w=0.02),
+    # d_model 16384 on the matrix cores: 16 input rows per thread, 8 batch
+    # rows per launch.
+    "bf16_i4_16384x320_b6": W.small_config(d=16384, f=320, batch=6, seed=15, in_frac=0.3,
+                                           sigma_w=0.01),
     # Maximum sizes: d_model 16384 (16 input rows per thread, 2 batch rows
     # per proxy launch) and d_ff 65536 (64 score rows per thread).
     "bf16_i4_16384x320_b3": W.small_config(d=16384, f=320, batch=3, seed=10, in_frac=0.3,

@@ -156,22 +156,25 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
         return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
     };
+    int pos[C];   // list position of each of this thread's inputs, -1 if not kept
 #pragma unroll
     for (int r = 0; r < C; ++r) {
         const int i = r * kBlock + tid;
-        if (i >= d) continue;
-        const bool s = (sel >> r) & 1;
-        if (tile == 0 && in_mask) in_mask[i] = s ? 1 : 0;
-        if (s) rows_sh[list_pos(r)] = (uint16_t)i;
+        const bool s = i < d && ((sel >> r) & 1);
+        pos[r] = s ? list_pos(r) : -1;
+        if (tile == 0 && in_mask && i < d) in_mask[i] = s ? 1 : 0;
+        if (s) rows_sh[pos[r]] = (uint16_t)i;
     }
-    for (int b = 0; b < NX; ++b) {
-        const uint16_t *xb = x_all + (size_t)(row0 + min(b, nb - 1)) * d;
+    // Only the nb real batch rows are stored: the stream feeds zeros for the
+    // others.
+    for (int b = 0; b < nb; ++b) {
+        const uint16_t *xb = x_all + (size_t)(row0 + b) * d;
+        uint16_t xv[C];
 #pragma unroll
-        for (int r = 0; r < C; ++r) {
-            const int i = r * kBlock + tid;
-            const uint16_t xv = xb[min(i, d - 1)];
-            if (i < d && ((sel >> r) & 1)) xs_sh[b * cap + list_pos(r)] = b < nb ? xv : (uint16_t)0;
-        }
+        for (int r = 0; r < C; ++r) xv[r] = xb[min(r * kBlock + tid, d - 1)];
+#pragma unroll
+        for (int r = 0; r < C; ++r)
+            if (pos[r] >= 0) xs_sh[b * cap + pos[r]] = xv[r];
     }
     __syncthreads();   // the kept rows are in place: pads copy the group's last one
     for (int g = tid; g < ng; g += kBlock) {
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         const int p0 = gstart[g], p1 = gstart[g + 1];
         for (int p = p0 + cnt; p < p1; ++p) {   // p1 > p0 + cnt only when cnt > 0
             rows_sh[p] = rows_sh[p0 + cnt - 1];
-            for (int b = 0; b < NX; ++b) xs_sh[b * cap + p] = 0;
+            for (int b = 0; b < nb; ++b) xs_sh[b * cap + p] = 0;
         }
         for (int kb = p0 / kMfmaBlock; kb < p1 / kMfmaBlock; ++kb) kbg_sh[kb] = (uint16_t)g;
     }
@@ -231,7 +234,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
                 const int k = min(kb + u, kb1 - 1);
                 const uint2 rr = *reinterpret_cast<const uint2 *>(rows_sh + k * kMfmaBlock + lg * 4);
                 const uint32_t r4[4] = {rr.x & 0xFFFFu, rr.x >> 16, rr.y & 0xFFFFu, rr.y >> 16};
-                xa[u] = ln < NX ? *reinterpret_cast<const uint2 *>(xs_sh + ln * cap + k * kMfmaBlock + lg * 4)
+                xa[u] = ln < nb ? *reinterpret_cast<const uint2 *>(xs_sh + ln * cap + k * kMfmaBlock + lg * 4)
                                 : make_uint2(0u, 0u);
                 gk[u] = kbg_sh[k];
 #pragma unroll

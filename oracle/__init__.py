@@ -57,6 +57,7 @@ def lib():
         L.oracle_select_channels.argtypes = [P, I, I, P]
         L.oracle_stage2.argtypes = [P, I, I, I, I, P, P, P, P, I, P, P, I]
         L.oracle_ffn_dense.argtypes = [P, I, I, I, I, P, P, P, P, I]
+        L.oracle_stage2_w4.argtypes = [P, I, I, I, I, P, P, P, P, P, P, P, I, P, P, I]
         L.oracle_ffn_sparse.argtypes = [P, I, I, I, I, P, P, P, I, P, P, P, P, I, I, I,
                                         P, P, P, P, P, I]
         L.oracle_add_rmsnorm.argtypes = [P, P, I, I, I, D, P]
@@ -169,6 +170,53 @@ def stage2(x, dtype: int, w_gate, w_up, w_down, ff_idx, act=SILU):
     lib().oracle_stage2(_p(x), dtype, B, d, f, _p(wg), _p(wu), _p(wd), _p(ff_idx),
                         ff_idx.size, _p(s), _p(y), act)
     return s[:, :ff_idx.size], y
+
+
+def stage2_w4(x, dtype: int, w4, ff_idx, act=SILU):
+    """Stage 2 on INT4 base weights (W4A16; Sec. 5.1 names the combination
+    as future work).  w4 = dict(codes_g, scales_g, codes_u, scales_u, codes_d,
+    scales_d, group): each matrix as quantize(w, dtype, 4, group) returns it.
+    Returns (s [B][k_ff], y [B][d]) in fp64."""
+    x = _u16(np.atleast_2d(x))
+    B, d = x.shape
+    c = {k: np.ascontiguousarray(w4[k], np.int8) for k in ("codes_g", "codes_u", "codes_d")}
+    sc = {k: _u16(w4[k]) for k in ("scales_g", "scales_u", "scales_d")}
+    ff_idx = np.ascontiguousarray(ff_idx, dtype=np.int32)
+    s = np.empty((B, max(ff_idx.size, 1)))
+    y = np.empty((B, d))
+    lib().oracle_stage2_w4(_p(x), dtype, B, d, int(w4["group"]), _p(c["codes_g"]),
+                           _p(sc["scales_g"]), _p(c["codes_u"]), _p(sc["scales_u"]),
+                           _p(c["codes_d"]), _p(sc["scales_d"]), _p(ff_idx), ff_idx.size,
+                           _p(s), _p(y), act)
+    return s[:, :ff_idx.size], y
+
+
+def quantize_w4(w_gate, w_up, w_down, dtype: int, group: int) -> dict:
+    """The three base matrices in the 4-bit group format stage2_w4 takes."""
+    out = {"group": group}
+    for key, w in (("g", w_gate), ("u", w_up), ("d", w_down)):
+        out["codes_" + key], out["scales_" + key] = quantize(w, dtype, 4, group)
+    return out
+
+
+def ffn_dense_w4(x, dtype: int, w4, act=SILU):
+    """The dense FFN on INT4 base weights: stage2_w4 over every channel."""
+    f = np.asarray(w4["codes_g"]).shape[0]
+    return stage2_w4(x, dtype, w4, np.arange(f, dtype=np.int32), act)[1]
+
+
+def ffn_sparse_w4(x, dtype: int, w4, k_in: int, k_ff: int, *, codes_g, scales_g, codes_u,
+                  scales_u, group: int, act=SILU):
+    """The Sec. 4.1 decode step with Stage 2 on INT4 base weights: input
+    top-k, the INT4 proxy score, channel top-k, then stage2_w4.  The proxy
+    arguments are those of proxy() (a proxy of the original weights).
+    Returns dict(y, in_idx, score, ff_idx)."""
+    in_idx = select_inputs(x, dtype, k_in)
+    _, _, _, score = proxy(x, dtype, in_idx, codes_g=codes_g, scales_g=scales_g,
+                           codes_u=codes_u, scales_u=scales_u, group=group, act=act)
+    ff_idx = select_channels(score, k_ff)
+    _, y = stage2_w4(x, dtype, w4, ff_idx, act)
+    return {"y": y, "in_idx": in_idx, "score": score, "ff_idx": ff_idx}
 
 
 def ffn_dense(x, dtype: int, w_gate, w_up, w_down, act=SILU):

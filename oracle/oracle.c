@@ -192,6 +192,68 @@ void oracle_quantize(const uint16_t *w, int dtype, int d, int f, int bits, int g
 }
 
 /* ------------------------------------------------------------------ */
+/* Stage 2 on INT4 base weights (W4A16)                                 */
+/* ------------------------------------------------------------------ */
+
+/*
+ * Low-bit base weights combined with the sparse step, which the paper leaves
+ * to future work (Sec. 5.1, compatibility with model quantization).  Each of
+ * W_gate, W_up, W_down is stored as the symmetric 4-bit group quantisation of
+ * Sec. 4.3 (oracle_quantize with bits = 4): entry (j, i) stands for
+ * sigma_{j,g(i)} * q_{j,i}, g(i) = i / group.
+ * Gate and up sum x_i q_{j,i} over each group and scale each group sum once;
+ * the down row j scales q_{j,c} by the sigma of output column c's group.
+ * Codes are int8 [f][d], scales fp16 bits [f][d/group].  Otherwise the step
+ * is oracle_stage2: s_{b,j} = act(g_{b,j}) u_{b,j}, y_b = sum_j s_{b,j} W_down[j, :].
+ */
+void oracle_stage2_w4(const uint16_t *x, int dtype, int B, int d, int group,
+                      const int8_t *cg, const uint16_t *sg, const int8_t *cu,
+                      const uint16_t *su, const int8_t *cd, const uint16_t *sd,
+                      const int32_t *ff_idx, int k_ff, double *s_out, double *y, int act)
+{
+    const int ng = d / group;
+    double *s = (double *)malloc(sizeof(double) * (size_t)B * (size_t)(k_ff > 0 ? k_ff : 1));
+#pragma omp parallel for schedule(static)
+    for (int t = 0; t < k_ff; ++t) {
+        int j = ff_idx[t];
+        for (int b = 0; b < B; ++b) {
+            double g = 0.0, u = 0.0;
+            for (int gr = 0; gr < ng; ++gr) {
+                double gq = 0.0, uq = 0.0;   /* sum of x_i q_{j,i} over the group */
+                for (int i = gr * group; i < (gr + 1) * group; ++i) {
+                    double xi = XV(b, i);
+                    gq += xi * (double)cg[(size_t)j * d + i];
+                    uq += xi * (double)cu[(size_t)j * d + i];
+                }
+                g += f16_to_double(sg[(size_t)j * ng + gr]) * gq;
+                u += f16_to_double(su[(size_t)j * ng + gr]) * uq;
+            }
+            s[(size_t)b * k_ff + t] = oracle_gate_act(g, act) * u;
+        }
+    }
+    const int cblk = 256;
+#pragma omp parallel for schedule(static)
+    for (int c0 = 0; c0 < d; c0 += cblk) {
+        int c1 = c0 + cblk < d ? c0 + cblk : d;
+        for (int b = 0; b < B; ++b) {
+            double *yb = y + (size_t)b * d;
+            for (int c = c0; c < c1; ++c)
+                yb[c] = 0.0;
+            for (int t = 0; t < k_ff; ++t) {
+                int j = ff_idx[t];
+                double sj = s[(size_t)b * k_ff + t];
+                for (int c = c0; c < c1; ++c)
+                    yb[c] += sj * f16_to_double(sd[(size_t)j * ng + c / group]) *
+                             (double)cd[(size_t)j * d + c];
+            }
+        }
+    }
+    if (s_out)
+        memcpy(s_out, s, sizeof(double) * (size_t)B * (size_t)k_ff);
+    free(s);
+}
+
+/* ------------------------------------------------------------------ */
 /* Top-k selection (App. A.6, per-token top-k rule)                     */
 /* ------------------------------------------------------------------ */
 

@@ -203,6 +203,61 @@ prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, c
 const char *prox_sparse_stage_name(int i);
 
 /*
+ * Low-bit base weights combined with the sparse step (W4A16): Sec. 5.1 finds
+ * the two complementary and leaves kernels that do both to future work.
+ * Stage 2 reads an INT4 copy of W_gate, W_up and W_down instead of the 16-bit
+ * rows; Stage 1 is unchanged (the proxy is packed from the 16-bit weights as
+ * usual).  Each matrix is quantised like the proxy (Sec. 4.3): per (channel,
+ * group of `group` consecutive inputs along d_model) a scale sigma = amax / 7
+ * rounded to fp16, codes q = round-half-even(w / sigma) clamped to [-7, 7],
+ * so the weight (j, i) stands for sigma_{j,g(i)} q_{j,i}.  Stage 2 computes
+ *   g_j = sum_g sigma^gate_{j,g} sum_{i in g} x_i q^gate_{j,i}   (u_j alike),
+ *   y   = sum_{j in m_s} s_j sum_c sigma^down_{j,g(c)} q^down_{j,c} e_c,
+ * with fp32 accumulation, y rounded once to the dtype.
+ * The blob (device, 256-byte aligned, prox_w4_bytes() bytes) holds, for
+ * gate, up and down in turn, the codes [d_ff][d_model / 2] (input i of
+ * channel j in byte i / 2: the low nibble when i is even, as q + 8), then the
+ * three scale arrays [d_ff][d_model / group] of fp16 bit patterns; every
+ * array starts on a 256-byte boundary.  All fields are inputs.
+ */
+typedef struct {
+    int dtype;     /* prox_dtype of x and y (and of the weights packed from) */
+    int d_model;
+    int d_ff;
+    int group;     /* a multiple of 128 that divides d_model */
+    int act;       /* prox_act */
+    void *blob;
+    size_t bytes;
+} prox_w4_weights;
+
+/* Bytes of the W4 blob for this shape; 0 if unsupported. */
+size_t prox_w4_bytes(int d_model, int d_ff, int group);
+
+/* Quantise w's three matrices into q->blob (bit-exact, deterministic).
+ * q->dtype, d_model, d_ff must equal w's. */
+prox_status prox_pack_w4(const prox_weights *w, const prox_w4_weights *q, hipStream_t stream);
+
+/* Inverse view of matrix 0 (gate), 1 (up) or 2 (down), for inspection and
+ * tests: codes int8 [d_ff][d_model] and scales [d_ff][d_model / group],
+ * both device pointers. */
+prox_status prox_unpack_w4(const prox_w4_weights *q, int matrix, int8_t *codes,
+                           uint16_t *scales, hipStream_t stream);
+
+/* The dense FFN on the INT4 weights (every channel; the W4 baseline).
+ * x, y, batch, ws, ws_bytes as prox_ffn_dense. */
+prox_status prox_ffn_dense_w4(const prox_w4_weights *q, const void *x, int batch, void *y,
+                              void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* The sparse decode step of prox_ffn_sparse with Stage 2 on the INT4 weights.
+ * p is the proxy of the same FFN.  events: NULL, or PROX_SPARSE_STAGES + 1
+ * caller-created events recorded as in prox_ffn_sparse_staged.  Other
+ * arguments as prox_ffn_sparse. */
+prox_status prox_ffn_sparse_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
+                               int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                               uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                               hipEvent_t *events, hipStream_t stream);
+
+/*
  * Threshold calibration (App. A.7), host code only (no HIP calls; all
  * pointers are host memory).  Offline, a layer's thresholds come from
  * calibration activations run through the earlier layers with their final

@@ -39,6 +39,39 @@ prox_status check_weights(const prox_weights *w) {
     return PROX_OK;
 }
 
+bool w4_group_ok(int d, int group) { return group >= 128 && group % 128 == 0 && d % group == 0; }
+
+prox_status check_w4(const prox_w4_weights *q) {
+    if (!q || !q->blob || !aligned(q->blob, 256)) return PROX_ERR_INVALID;
+    if (!dtype_ok(q->dtype)) return PROX_ERR_INVALID;
+    if (q->act != PROX_ACT_SILU && q->act != PROX_ACT_GELU) return PROX_ERR_INVALID;
+    if (q->d_model < 1 || q->d_ff < 1) return PROX_ERR_INVALID;
+    if (!shape_ok(q->d_model, q->d_ff) || !w4_group_ok(q->d_model, q->group))
+        return PROX_ERR_UNSUPPORTED;
+    if (q->bytes < W4Layout(q->d_model, q->d_ff, q->group).total) return PROX_ERR_WORKSPACE;
+    return PROX_OK;
+}
+
+// What the launch sequence needs of either weight format.
+struct Model {
+    int dtype, d, f, act;
+    Stage2Weights s2;
+};
+
+Model model_of(const prox_weights *w) {
+    return Model{w->dtype, w->d_model, w->d_ff, w->act,
+                 Stage2Weights{w->w_gate, w->w_up, w->w_down, nullptr, nullptr, nullptr, 16, 0}};
+}
+
+Model model_of(const prox_w4_weights *q) {
+    const W4Layout L(q->d_model, q->d_ff, q->group);
+    const uint8_t *b = static_cast<const uint8_t *>(q->blob);
+    auto sc = [&](int m) { return reinterpret_cast<const uint16_t *>(b + L.scales[m]); };
+    return Model{q->dtype, q->d_model, q->d_ff, q->act,
+                 Stage2Weights{b + L.codes[0], b + L.codes[1], b + L.codes[2], sc(0), sc(1), sc(2), 4,
+                               q->group}};
+}
+
 prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_ERR_HIP; }
 
 #define PROX_TRY(expr)                                \
@@ -65,21 +98,21 @@ const char *const kStageNames[PROX_SPARSE_STAGES] = {"proxy_gemv_score",
 
 // Stage 2 and the final reduction, shared by the sparse and the dense FFN
 // (scores == NULL: every channel).
-prox_status stage2_and_reduce(const prox_weights *w, const void *x, int batch, int k_ff,
+prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff,
                               const float *scores, uint8_t *mask, float *scores_copy, void *y,
                               const Ws &W, Select sel, hipEvent_t *events, hipStream_t stream) {
-    const int d = w->d_model, f = w->d_ff, dt = w->dtype;
+    const int d = m.d, f = m.f, dt = m.dtype;
     const uint16_t *xb = static_cast<const uint16_t *>(x);
     // With the threshold rule the kept count is found on the device: size the
     // grid for every channel (workgroups past the count get no channels).
     const int nwg = stage2_wgs(scores && !sel.tau_mode ? k_ff : f);
     const int ystride = ypart_rows(batch);
-    for (int c0 = 0; c0 < batch; c0 += kStage2MaxNB) {
-        const int nb = batch - c0 < kStage2MaxNB ? batch - c0 : kStage2MaxNB;
-        PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, w->w_gate, w->w_up, w->w_down,
-                               scores, k_ff, mask, c0 == 0 ? scores_copy : nullptr,
-                               W.ypart + (size_t)c0 * d, ystride, nwg,
-                               c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, w->act,
+    const int rows = stage2_rows(d, m.s2.wq);
+    for (int c0 = 0; c0 < batch; c0 += rows) {
+        const int nb = batch - c0 < rows ? batch - c0 : rows;
+        PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
+                               c0 == 0 ? scores_copy : nullptr, W.ypart + (size_t)c0 * d, ystride,
+                               nwg, c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, m.act,
                                stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
@@ -100,17 +133,15 @@ struct Rules {
     int32_t *counts;   // threshold mode: [k_in, k_ff] realised, or NULL
 };
 
-prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
+prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int batch,
                         int k_in, int k_ff, const Rules &rules, void *y, uint8_t *mask,
                         uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
                         hipEvent_t *events, hipStream_t stream) {
-    prox_status st = check_weights(w);
-    if (st != PROX_OK) return st;
     if (!p || !p->blob || !x || !y || !mask || !ws) return PROX_ERR_INVALID;
     if (!aligned(x, 16) || !aligned(y, 16) || !aligned(p->blob, 16) || !aligned(ws, 256) ||
         (scores && !aligned(scores, 4)))
         return PROX_ERR_INVALID;
-    const int d = w->d_model, f = w->d_ff;
+    const int d = m.d, f = m.f;
     if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
     if (rules.tau_mode) {
         if (std::isnan(rules.tau_x) || std::isnan(rules.tau_s)) return PROX_ERR_INVALID;
@@ -129,7 +160,7 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
             if (!events[i]) return PROX_ERR_INVALID;
 
     const Ws W = carve(ws, d, f, batch);
-    const int dt = w->dtype;
+    const int dt = m.dtype;
     if (events) PROX_TRY(hipEventRecord(events[0], stream));
     // Several batch rows with an INT4 proxy: the matrix-core kernel, which
     // reads the codes once for up to 16 rows; else the dot-product kernel.
@@ -141,16 +172,27 @@ prox_status sparse_impl(const prox_weights *w, const prox_proxy *p, const void *
         if (mfma_rows)
             PROX_TRY(launch_proxy_mfma(dt, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
                                        c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel,
-                                       w->act, stream));
+                                       m.act, stream));
         else
             PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
-                                  c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, w->act,
+                                  c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, m.act,
                                   stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[1], stream));
     const Select ff_sel{rules.tau_mode, rules.tau_s, rules.counts ? rules.counts + 1 : nullptr};
-    return stage2_and_reduce(w, x, batch, k_ff, W.scores, mask, scores, y, W, ff_sel, events,
+    return stage2_and_reduce(m, x, batch, k_ff, W.scores, mask, scores, y, W, ff_sel, events,
                              stream);
+}
+
+prox_status dense_impl(const Model &m, const void *x, int batch, void *y, void *ws,
+                       size_t ws_bytes, hipStream_t stream) {
+    if (!x || !y || !ws) return PROX_ERR_INVALID;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 256)) return PROX_ERR_INVALID;
+    if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
+    if (ws_bytes < WsLayout(m.d, m.f, batch).total) return PROX_ERR_WORKSPACE;
+    const Ws W = carve(ws, m.d, m.f, batch);
+    return stage2_and_reduce(m, x, batch, m.f, nullptr, nullptr, nullptr, y, W,
+                             Select{0, 0.0f, nullptr}, nullptr, stream);
 }
 
 }  // namespace
@@ -221,29 +263,26 @@ prox_status prox_ffn_dense(const prox_weights *w, const void *x, int batch, void
                            size_t ws_bytes, hipStream_t stream) {
     prox_status st = check_weights(w);
     if (st != PROX_OK) return st;
-    if (!x || !y || !ws) return PROX_ERR_INVALID;
-    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 256)) return PROX_ERR_INVALID;
-    if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
-    const int d = w->d_model, f = w->d_ff;
-    if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
-    const Ws W = carve(ws, d, f, batch);
-    return stage2_and_reduce(w, x, batch, f, nullptr, nullptr, nullptr, y, W,
-                             Select{0, 0.0f, nullptr}, nullptr, stream);
+    return dense_impl(model_of(w), x, batch, y, ws, ws_bytes, stream);
 }
 
 prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const void *x, int batch,
                             int k_in, int k_ff, void *y, uint8_t *mask, uint8_t *in_mask,
                             float *scores, void *ws, size_t ws_bytes, hipStream_t stream) {
-    return sparse_impl(w, p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y, mask,
-                       in_mask, scores, ws, ws_bytes, nullptr, stream);
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    return sparse_impl(model_of(w), p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y,
+                       mask, in_mask, scores, ws, ws_bytes, nullptr, stream);
 }
 
 prox_status prox_ffn_sparse_tau(const prox_weights *w, const prox_proxy *p, const void *x,
                                 int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
                                 uint8_t *in_mask, float *scores, int32_t *counts, void *ws,
                                 size_t ws_bytes, hipStream_t stream) {
-    return sparse_impl(w, p, x, batch, 0, 0, Rules{1, tau_x, tau_s, counts}, y, mask, in_mask,
-                       scores, ws, ws_bytes, nullptr, stream);
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    return sparse_impl(model_of(w), p, x, batch, 0, 0, Rules{1, tau_x, tau_s, counts}, y, mask,
+                       in_mask, scores, ws, ws_bytes, nullptr, stream);
 }
 
 prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, const void *x,
@@ -251,8 +290,53 @@ prox_status prox_ffn_sparse_staged(const prox_weights *w, const prox_proxy *p, c
                                    uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
                                    hipEvent_t *events, hipStream_t stream) {
     if (!events) return PROX_ERR_INVALID;
-    return sparse_impl(w, p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y, mask,
-                       in_mask, scores, ws, ws_bytes, events, stream);
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    return sparse_impl(model_of(w), p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y,
+                       mask, in_mask, scores, ws, ws_bytes, events, stream);
+}
+
+size_t prox_w4_bytes(int d_model, int d_ff, int group) {
+    if (!shape_ok(d_model, d_ff) || !w4_group_ok(d_model, group)) return 0;
+    return W4Layout(d_model, d_ff, group).total;
+}
+
+prox_status prox_pack_w4(const prox_weights *w, const prox_w4_weights *q, hipStream_t stream) {
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    st = check_w4(q);
+    if (st != PROX_OK) return st;
+    if (q->dtype != w->dtype || q->d_model != w->d_model || q->d_ff != w->d_ff)
+        return PROX_ERR_INVALID;
+    return hip_status(launch_pack_w4(w->dtype, w->w_gate, w->w_up, w->w_down, w->d_model,
+                                     w->d_ff, q->group, q->blob, stream));
+}
+
+prox_status prox_unpack_w4(const prox_w4_weights *q, int matrix, int8_t *codes,
+                           uint16_t *scales, hipStream_t stream) {
+    prox_status st = check_w4(q);
+    if (st != PROX_OK) return st;
+    if (matrix < 0 || matrix > 2 || !codes || !scales || !aligned(scales, 2))
+        return PROX_ERR_INVALID;
+    return hip_status(launch_unpack_w4(q->blob, q->d_model, q->d_ff, q->group, matrix, codes,
+                                       scales, stream));
+}
+
+prox_status prox_ffn_dense_w4(const prox_w4_weights *q, const void *x, int batch, void *y,
+                              void *ws, size_t ws_bytes, hipStream_t stream) {
+    prox_status st = check_w4(q);
+    if (st != PROX_OK) return st;
+    return dense_impl(model_of(q), x, batch, y, ws, ws_bytes, stream);
+}
+
+prox_status prox_ffn_sparse_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
+                               int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                               uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                               hipEvent_t *events, hipStream_t stream) {
+    prox_status st = check_w4(q);
+    if (st != PROX_OK) return st;
+    return sparse_impl(model_of(q), p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y,
+                       mask, in_mask, scores, ws, ws_bytes, events, stream);
 }
 
 prox_status prox_add_rmsnorm(const void *x, const void *y, int batch, int d_model,

@@ -67,6 +67,24 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
                                       c, false);
 }
 
+// INT4 dequant by exponent OR: a nibble n under the bits of M (128.0 in bf16,
+// 1024.0 in fp16) is exactly the 16-bit value M + n, so a code q stored as
+// n = q + 8 reads back as q after subtracting offset = M + 8 once per sum.
+template <int DT>
+struct Int4Magic;
+template <>
+struct Int4Magic<kBF16> {
+    static constexpr uint32_t pair = 0x43004300u;   // (128.0, 128.0)
+    static constexpr uint32_t one = 0x3F803F80u;    // (1.0, 1.0)
+    static constexpr float offset = 136.0f;
+};
+template <>
+struct Int4Magic<kF16> {
+    static constexpr uint32_t pair = 0x64006400u;   // (1024.0, 1024.0)
+    static constexpr uint32_t one = 0x3C003C00u;
+    static constexpr float offset = 1032.0f;
+};
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // 16-byte streaming load (non-temporal hint: weights are read once per call).

@@ -34,15 +34,32 @@ hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, 
                              hipStream_t stream);
 constexpr int kProxyMfmaMinRows = 5;   // batch rows from which Stage 1 uses the matrix cores
 
+// The three matrices of Stage 2: channel-major 16-bit rows (wq == 16), or
+// INT4 codes with fp16 scales per (channel, group along d), laid out as
+// W4Layout describes (wq == 4).
+struct Stage2Weights {
+    const void *wg, *wu, *wd;
+    const uint16_t *sg, *su, *sd;   // INT4 scales, else unused
+    int wq, group;
+};
+// Batch rows one Stage 2 launch takes: kStage2MaxNB, fewer with INT4 weights
+// when d is wide (their launch keeps all nb rows of x in LDS).
+int stage2_rows(int d, int wq);
 // act (both stages): the gate activation, 0 SiLU or 1 GELU.
-// Stage 2 for batch rows x[0..nb) (nb <= kStage2MaxNB).  scores == NULL runs
-// the dense FFN over all f channels; otherwise the top k_ff scores, or the
-// threshold rule of sel, pick the channels.  Partial y rows go to
+// Stage 2 for batch rows x[0..nb) (nb <= stage2_rows(d, w.wq)).  scores ==
+// NULL runs the dense FFN over all f channels; otherwise the top k_ff scores,
+// or the threshold rule of sel, pick the channels.  Partial y rows go to
 // ypart[(w * ystride + b) * d + c] for workgroup w < nwg.
-hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
-                         const void *wu, const void *wd, const float *scores, int k_ff,
-                         uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, Select sel, int act, hipStream_t stream);
+hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const Stage2Weights &w,
+                         const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
+                         float *ypart, int ystride, int nwg, Select sel, int act,
+                         hipStream_t stream);
+// INT4 base weights: quantise W_gate, W_up, W_down (channel-major [f][d]) into
+// a W4Layout blob, and the inverse view of matrix m (0 gate, 1 up, 2 down).
+hipError_t launch_pack_w4(int dtype, const void *wg, const void *wu, const void *wd, int d, int f,
+                          int group, void *blob, hipStream_t stream);
+hipError_t launch_unpack_w4(const void *blob, int d, int f, int group, int m, int8_t *codes,
+                            uint16_t *scales, hipStream_t stream);
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,
                          hipStream_t stream);
 hipError_t launch_add_rmsnorm(int dtype, const void *x, const void *y, int batch, int d, float eps,

@@ -86,6 +86,26 @@ __host__ __device__ inline int stage2_wgs(int n_ch) {
     return w < 1 ? 1 : (w > kStage2MaxWGs ? kStage2MaxWGs : w);
 }
 
+// INT4 base weights for Stage 2 (W4A16).  For each matrix m (gate, up, down),
+// channel-major codes [f][d/2] (column i of row j in byte i/2: the low nibble
+// when i is even, as q + 8) and fp16 scales [f][d/group]; every array starts
+// on a 256-byte boundary.
+struct W4Layout {
+    size_t codes[3], scales[3], total;
+    __host__ __device__ W4Layout(int d, int f, int group) {
+        size_t off = 0;
+        for (int m = 0; m < 3; ++m) {
+            codes[m] = off;
+            off = align_up(off + (size_t)f * (size_t)(d / 2), 256);
+        }
+        for (int m = 0; m < 3; ++m) {
+            scales[m] = off;
+            off = align_up(off + (size_t)f * (size_t)(d / group) * 2, 256);
+        }
+        total = off;
+    }
+};
+
 constexpr int kStage2MaxNB = 8;          // batch rows per Stage 2 launch
 
 // Batch rows a Stage 2 launch of nb <= 8 rows is compiled for (1, 2, 4 or 8).

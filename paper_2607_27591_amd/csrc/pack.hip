@@ -157,6 +157,85 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint8_t *__restrict__
     }
 }
 
+// INT4 base weights (W4A16): one thread per (matrix, channel, group), the
+// same symmetric quantiser as the proxy (scale = amax / 7 rounded to fp16,
+// q = round-half-even of w / scale in fp64, clamped to +-7), stored
+// channel-major.
+template <int DT>
+__global__ __launch_bounds__(256) void pack_w4_kernel(const uint16_t *__restrict__ wg,
+                                                      const uint16_t *__restrict__ wu,
+                                                      const uint16_t *__restrict__ wd, int d, int f,
+                                                      int group, uint8_t *__restrict__ blob) {
+    const W4Layout L(d, f, group);
+    const int ng = d / group;
+    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= 3LL * f * ng) return;
+    const int m = (int)(gid / ((long long)f * ng));
+    const int rem = (int)(gid % ((long long)f * ng));
+    const int j = rem / ng, g = rem % ng;
+    const uint16_t *w = (m == 0 ? wg : m == 1 ? wu : wd) + (size_t)j * d + (size_t)g * group;
+    double amax = 0.0;
+    for (int i = 0; i < group; ++i) amax = fmax(amax, fabs(w_to_f64<DT>(w[i])));
+    const uint16_t sbits = f64_to_f16_rne(amax / 7.0);
+    const double sigma = f16_to_f64(sbits);
+    reinterpret_cast<uint16_t *>(blob + L.scales[m])[(size_t)j * ng + g] = sbits;
+    uint8_t *codes = blob + L.codes[m] + (size_t)j * (d / 2) + (size_t)g * (group / 2);
+    for (int i = 0; i < group; i += 2) {
+        int q[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            q[e] = 0;
+            if (sigma != 0.0) {
+                const double r = rint(w_to_f64<DT>(w[i + e]) / sigma);
+                q[e] = (int)fmin(fmax(r, -7.0), 7.0);
+            }
+        }
+        codes[i / 2] = (uint8_t)((q[0] + 8) | ((q[1] + 8) << 4));
+    }
+}
+
+// Inverse view of matrix m: codes int8 [f][d] and scales [f][d/group].
+__global__ __launch_bounds__(256) void unpack_w4_kernel(const uint8_t *__restrict__ blob, int d,
+                                                        int f, int group, int m, int8_t *codes,
+                                                        uint16_t *scales) {
+    const W4Layout L(d, f, group);
+    const int ng = d / group;
+    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= (long long)f * ng) return;
+    const int j = (int)(gid / ng), g = (int)(gid % ng);
+    scales[(size_t)j * ng + g] =
+        reinterpret_cast<const uint16_t *>(blob + L.scales[m])[(size_t)j * ng + g];
+    const uint8_t *src = blob + L.codes[m] + (size_t)j * (d / 2) + (size_t)g * (group / 2);
+    int8_t *out = codes + (size_t)j * d + (size_t)g * group;
+    for (int i = 0; i < group; i += 2) {
+        const uint8_t byte = src[i / 2];
+        out[i] = (int8_t)((int)(byte & 15) - 8);
+        out[i + 1] = (int8_t)((int)(byte >> 4) - 8);
+    }
+}
+
+hipError_t launch_pack_w4(int dtype, const void *wg, const void *wu, const void *wd, int d, int f,
+                          int group, void *blob, hipStream_t s) {
+    const long long n = 3LL * f * (d / group);
+    const int nb = (int)((n + 255) / 256);
+    auto *g = static_cast<const uint16_t *>(wg);
+    auto *u = static_cast<const uint16_t *>(wu);
+    auto *dn = static_cast<const uint16_t *>(wd);
+    auto *b = static_cast<uint8_t *>(blob);
+    if (dtype == kBF16) pack_w4_kernel<kBF16><<<nb, 256, 0, s>>>(g, u, dn, d, f, group, b);
+    else pack_w4_kernel<kF16><<<nb, 256, 0, s>>>(g, u, dn, d, f, group, b);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_w4(const void *blob, int d, int f, int group, int m, int8_t *codes,
+                            uint16_t *scales, hipStream_t s) {
+    const long long n = (long long)f * (d / group);
+    const int nb = (int)((n + 255) / 256);
+    unpack_w4_kernel<<<nb, 256, 0, s>>>(static_cast<const uint8_t *>(blob), d, f, group, m,
+                                        codes, scales);
+    return hipGetLastError();
+}
+
 hipError_t launch_pack(int dtype, int qbits, const void *wg, const void *wu, int d, int f,
                        int group, void *blob, hipStream_t s) {
     const BlobLayout L(d, f, qbits, group);

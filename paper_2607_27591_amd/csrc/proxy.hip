@@ -24,23 +24,7 @@
 #include "kernels.hpp"
 #include "topk.hpp"
 
-
 namespace prox {
-
-template <int DT>
-struct Magic;
-template <>
-struct Magic<kBF16> {   // 0x4300 = 128.0 in bf16; 128 + n is exact for n < 128
-    static constexpr uint32_t pair = 0x43004300u;
-    static constexpr uint32_t one = 0x3F803F80u;   // (1.0, 1.0)
-    static constexpr float offset = 136.0f;   // 128 + 8 (code bias)
-};
-template <>
-struct Magic<kF16> {    // 0x6400 = 1024.0 in fp16; 1024 + n is exact for n < 1024
-    static constexpr uint32_t pair = 0x64006400u;
-    static constexpr uint32_t one = 0x3C003C00u;   // (1.0, 1.0)
-    static constexpr float offset = 1032.0f;
-};
 
 // (v & mask) | bits.  FUSED: one v_and_or_b32 (the compiler otherwise emits
 // two VOP2 instructions with literals); the asm form lengthens live ranges, so
@@ -61,7 +45,7 @@ __device__ __forceinline__ uint32_t and_or(uint32_t v, uint32_t mask, uint32_t b
 template <int DT, bool FUSED>
 __device__ __forceinline__ void int4_pair_dot8(uint32_t a, uint32_t b, uint32_t xpair,
                                                float *acc) {
-    constexpr uint32_t M = Magic<DT>::pair;
+    constexpr uint32_t M = Int4Magic<DT>::pair;
     constexpr uint32_t K = 0x000F000Fu;
     const uint32_t p = __builtin_amdgcn_perm(b, a, 0x05040100u);  // a.b0 a.b1 b.b0 b.b1
     const uint32_t q = __builtin_amdgcn_perm(b, a, 0x07060302u);  // a.b2 a.b3 b.b2 b.b3
@@ -157,7 +141,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     constexpr int SZ = CPL / 8;                   // uint4 of scales per lane and group
     constexpr bool kEarlyX = NB <= 2;             // projected x loaded with the keys
     constexpr bool kHoistX = NB == 1;             // x pairs read with the code loads
-    constexpr float off = QB == 4 ? Magic<DT>::offset : QB == 8 ? 128.0f : 0.0f;   // code bias
+    constexpr float off = QB == 4 ? Int4Magic<DT>::offset : QB == 8 ? 128.0f : 0.0f;   // code bias
     using W = typename ProxyLoad<QB, CPL>::type;
     const BlobLayout L(d, f, QB, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
@@ -384,7 +368,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                         if constexpr (kHoistX) xp = p < pb ? xpre[u] : 0u;
                         else xp = p < pb ? xs32[b * (cap / 2) + p] : 0u;
                         pair_accumulate<DT, QB, CPL, (NB <= 2)>(wa[u], wb[u], xp, acc[b]);
-                        xs[b] = dot2<DT>(xp, Magic<DT>::one, xs[b]);
+                        xs[b] = dot2<DT>(xp, Int4Magic<DT>::one, xs[b]);
                     }
                 }
             }

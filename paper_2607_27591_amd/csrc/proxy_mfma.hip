@@ -38,20 +38,6 @@ typedef unsigned short us2 __attribute__((ext_vector_type(2)));   // two rows' c
 constexpr int kMfmaBlock = 16;    // kept input rows per block (the MFMA's K)
 constexpr int kMfmaU = 4;         // blocks in flight per wave
 
-template <int DT>
-struct MfmaMagic;
-template <>
-struct MfmaMagic<kBF16> {   // 128.0 in bf16; 128 + n is exact for n < 128
-    static constexpr uint32_t pair = 0x43004300u;
-    static constexpr uint32_t ones = 0x3F803F80u;   // (1.0, 1.0)
-    static constexpr float offset = 136.0f;   // M + 8 (the code bias)
-};
-template <>
-struct MfmaMagic<kF16> {    // 1024.0 in fp16; 1024 + n is exact for n < 1024
-    static constexpr uint32_t pair = 0x64006400u;
-    static constexpr uint32_t ones = 0x3C003C00u;
-    static constexpr float offset = 1032.0f;
-};
 
 template <int DT>
 __device__ __forceinline__ v4f mfma16(uint2 a, uint2 b, v4f c) {
@@ -88,8 +74,8 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     static_assert(NX == 8 || NX == 16, "x rows kept in LDS");
     constexpr int WH = T / 64;                       // 64-column halves per tile
     constexpr int WPG = kMaxBlockWaves / (WH * 2);   // waves per (half, matrix)
-    constexpr uint32_t M = MfmaMagic<DT>::pair;
-    constexpr float off = MfmaMagic<DT>::offset;
+    constexpr uint32_t M = Int4Magic<DT>::pair;
+    constexpr float off = Int4Magic<DT>::offset;
     const BlobLayout L(d, f, 4, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
     const int tile = blockIdx.x;
@@ -207,7 +193,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         tot[c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
     }
     v4f xacc = v4f{0.0f, 0.0f, 0.0f, 0.0f};   // x sums of this wave's blocks, current group
-    const uint2 ones = make_uint2(MfmaMagic<DT>::ones, MfmaMagic<DT>::ones);
+    const uint2 ones = make_uint2(Int4Magic<DT>::one, Int4Magic<DT>::one);
 
     if (kb0 < kb1) {
         int gcur = kbg_sh[kb0];

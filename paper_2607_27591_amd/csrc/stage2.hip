@@ -24,10 +24,11 @@ namespace prox {
 constexpr int kMaxSlice = (kMaxDFF + kStage2MaxWGs - 1) / kStage2MaxWGs;   // channels per WG
 constexpr int kMaxParts = 8;
 
-// d is cut into Q parts for the gate/up units (each part >= 2048 columns).
-__host__ __device__ inline int gateup_parts(int d, int nbt) {
+// d is cut into Q parts for the gate/up units (each part >= 2048 columns of
+// 16-bit weights, >= 4096 of INT4 codes: at least two 16-byte loads per lane).
+__host__ __device__ inline int gateup_parts(int d, int nbt, int wq) {
     if (nbt > 2) return 1;
-    int q = d / 2048;
+    int q = d / (wq == 4 ? 4096 : 2048);
     return q < 1 ? 1 : (q > kMaxParts ? kMaxParts : q);
 }
 
@@ -40,9 +41,11 @@ __host__ __device__ inline int stage2_down_groups(int d, int nbt) {
     return (ncg >= kBlock || nbt > 4) ? 1 : kBlock / ncg;
 }
 
-// Dynamic LDS ahead of s: x (when staged) or the down reduction buffer.
-__host__ __device__ inline size_t stage2_head_bytes(int d, int nbt) {
-    const size_t xbytes = x_in_lds(d, nbt) ? (size_t)nbt * d * 2 : 0;
+// Dynamic LDS ahead of s: x (when staged; with INT4 weights as permuted
+// pairs plus the sum of every 32 inputs) or the down reduction buffer.
+__host__ __device__ inline size_t stage2_head_bytes(int d, int nbt, int wq) {
+    const size_t xbytes = x_in_lds(d, nbt) ? (size_t)nbt * d * 2 + (wq == 4 ? (size_t)nbt * (d / 32) * 4 : 0)
+                                           : 0;
     const size_t red = stage2_down_groups(d, nbt) > 1 ? (size_t)(d / 8) * nbt * 8 * 4 : 0;
     return xbytes > red ? xbytes : red;
 }
@@ -55,14 +58,18 @@ struct Stage2Smem {
     float gu[kMaxSlice * kMaxParts * 2 * 2];   // [t][q][b][2] for nbt <= 2
 };
 
-template <int NB, int DT, int C>
+// WQ: 16 for 16-bit weights, 4 for INT4 codes (wt.sg/su/sd: their scales).
+template <int NB, int DT, int C, int WQ>
 __global__ __launch_bounds__(kBlock) void stage2_kernel(
-    const uint16_t *__restrict__ x, int nb, int d, int f, const uint16_t *__restrict__ wg,
-    const uint16_t *__restrict__ wu, const uint16_t *__restrict__ wd,
+    const uint16_t *__restrict__ x, int nb, int d, int f, Stage2Weights wt,
     const float *__restrict__ scores,   // NULL: dense FFN over all f channels
     int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
     float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
     Select sel_rule, int act) {                     // act: gate activation
+    static_assert(WQ == 16 || WQ == 4, "16-bit or INT4 weights");
+    const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
+    const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
+    const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
@@ -122,10 +129,30 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         for (int t = tid; t < n; t += kBlock) sm.list[t] = p0 + t;
     }
 
-    const bool xl = x_in_lds(d, NB);
+    const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
     uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
     const int nvec = d / 8;
-    if (xl) {
+    float *xsum = dyn + (size_t)NB * d / 2;   // INT4: [NB][d / 32] sums of x
+    if constexpr (WQ == 4) {
+        // x as pairs (x_{8m+k}, x_{8m+k+4}), k = 0..3, one uint4 per 8
+        // inputs: nibble k of a code word and nibble k + 4 sit in the low and
+        // high halves of (word >> 4k) & 0x000F000F, so one dot2 takes both.
+        for (int e = tid; e < NB * nvec; e += kBlock) {
+            const int b = e / nvec, vv = e % nvec;
+            const uint4 v = b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv]
+                                   : make_uint4(0, 0, 0, 0);
+            reinterpret_cast<uint4 *>(xs)[e] = make_uint4(
+                __builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
+                __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u));
+        }
+        for (int e = tid; e < NB * (d / 32); e += kBlock) {
+            const int b = e / (d / 32), c = e % (d / 32);
+            float sum = 0.0f;
+            if (b < nb)
+                for (int k = 0; k < 32; ++k) sum += half_to_float<DT>(x[(size_t)b * d + c * 32 + k]);
+            xsum[e] = sum;
+        }
+    } else if (xl) {
         for (int e = tid; e < NB * nvec; e += kBlock) {
             const int b = e / nvec, vv = e % nvec;
             reinterpret_cast<uint4 *>(xs)[e] =
@@ -135,9 +162,85 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     __syncthreads();
 
     // ---- gate/up: units (channel t, part q) over the 16 waves ----
-    const int Q = gateup_parts(d, NB);
+    const int Q = gateup_parts(d, NB, WQ);
+    float *s_sh = dyn + align_up(stage2_head_bytes(d, NB, WQ), 16) / 4;   // [slice][NB]
+    if constexpr (WQ == 4) {
+        // 16-byte code vectors (32 inputs, inside one group) per row.  Per
+        // vector and batch row: t = sum x_i (M + n_i) by dot2, then the group
+        // scale times (t - (M + 8) * sum x_i) into the row's total.
+        constexpr uint32_t M = Int4Magic<DT>::pair;
+        constexpr float off = Int4Magic<DT>::offset;
+        const int ng = d / wt.group;
+        const int nv4 = d / 32;
+        const int qv = nv4 / Q;
+        const uint4 *xs4 = reinterpret_cast<const uint4 *>(xs);
+        constexpr int U = 2;
+        for (int unit = wid; unit < n * Q; unit += kMaxBlockWaves) {
+            const int t = unit / Q, q = unit % Q;
+            const int j = sm.list[t];
+            const uint4 *rg = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(wt.wg) + (size_t)j * (d / 2));
+            const uint4 *ru = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(wt.wu) + (size_t)j * (d / 2));
+            const uint16_t *sgr = wt.sg + (size_t)j * ng, *sur = wt.su + (size_t)j * ng;
+            const int v_begin = q * qv, v_end = (q == Q - 1) ? nv4 : v_begin + qv;
+            float ag[NB], au[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) ag[b] = au[b] = 0.0f;
+            for (int v0 = v_begin + lane; v0 < v_end; v0 += kWave * U) {
+                uint4 gv[U], uv[U];
+                uint16_t gsb[U], usb[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int vv = v0 + u * kWave;
+                    if (vv < v_end) {
+                        gv[u] = load_stream16(rg + vv);
+                        uv[u] = load_stream16(ru + vv);
+                        gsb[u] = sgr[vv * 32 / wt.group];
+                        usb[u] = sur[vv * 32 / wt.group];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int vv = v0 + u * kWave;
+                    if (vv < v_end) {
+                        const float scg = f16_bits_to_float(gsb[u]), scu = f16_bits_to_float(usb[u]);
+                        const uint32_t cgw[4] = {gv[u].x, gv[u].y, gv[u].z, gv[u].w};
+                        const uint32_t cuw[4] = {uv[u].x, uv[u].y, uv[u].z, uv[u].w};
+#pragma unroll
+                        for (int b = 0; b < NB; ++b) {
+                            float tg = 0.0f, tu = 0.0f;
+#pragma unroll
+                            for (int w4 = 0; w4 < 4; ++w4) {
+                                const uint4 P = xs4[(size_t)b * nvec + vv * 4 + w4];
+                                const uint32_t pk[4] = {P.x, P.y, P.z, P.w};
+#pragma unroll
+                                for (int k = 0; k < 4; ++k) {
+                                    tg = dot2<DT>(pk[k], ((cgw[w4] >> (4 * k)) & 0x000F000Fu) | M, tg);
+                                    tu = dot2<DT>(pk[k], ((cuw[w4] >> (4 * k)) & 0x000F000Fu) | M, tu);
+                                }
+                            }
+                            const float xv = xsum[b * nv4 + vv];
+                            ag[b] = fmaf(scg, tg - off * xv, ag[b]);
+                            au[b] = fmaf(scu, tu - off * xv, au[b]);
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const float gs = wave_sum(ag[b]);
+                const float us = wave_sum(au[b]);
+                if (lane == 0) {
+                    if (Q == 1) {
+                        s_sh[t * NB + b] = gate_act(gs, act) * us;
+                    } else {
+                        sm.gu[((t * Q + q) * 2 + b) * 2 + 0] = gs;
+                        sm.gu[((t * Q + q) * 2 + b) * 2 + 1] = us;
+                    }
+                }
+            }
+        }
+    } else {
     const int qv = nvec / Q;                                   // 16-byte vectors per part
-    float *s_sh = dyn + align_up(stage2_head_bytes(d, NB), 16) / 4;   // [slice][NB]
     constexpr int U = 4;
     for (int unit = wid; unit < n * Q; unit += kMaxBlockWaves) {
         const int t = unit / Q, q = unit % Q;
@@ -193,6 +296,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
             }
         }
     }
+    }
     __syncthreads();
     if (Q > 1) {
         for (int e = tid; e < n * NB; e += kBlock) {
@@ -225,7 +329,43 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
-        if (active) {
+        if constexpr (WQ == 4) {
+            // 8 columns per thread: one 32-bit code word and the scale of
+            // their group per channel row.
+            const int ng = d / wt.group;
+            if (active) {
+                for (int t0 = gi; t0 < n; t0 += G * UD) {
+                    uint32_t cw[UD];
+                    uint16_t sb[UD];
+#pragma unroll
+                    for (int u = 0; u < UD; ++u) {
+                        const int t = t0 + u * G;
+                        if (t < n) {
+                            const int j = sm.list[t];
+                            cw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(
+                                static_cast<const uint8_t *>(wt.wd) + (size_t)j * (d / 2) + cg * 4));
+                            sb[u] = wt.sd[(size_t)j * ng + cg * 8 / wt.group];
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < UD; ++u) {
+                        const int t = t0 + u * G;
+                        if (t < n) {
+                            const float sc = f16_bits_to_float(sb[u]);
+                            float wf[8];
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) wf[e] = (float)(int)((cw[u] >> (4 * e)) & 15u) - 8.0f;
+#pragma unroll
+                            for (int b = 0; b < NB; ++b) {
+                                const float sv = s_sh[t * NB + b] * sc;
+#pragma unroll
+                                for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
+                            }
+                        }
+                    }
+                }
+            }
+        } else if (active) {
             for (int t0 = gi; t0 < n; t0 += G * UD) {
                 uint4 wv[UD];
 #pragma unroll
@@ -356,8 +496,15 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(const uint16_t *__res
 // Launchers
 // ---------------------------------------------------------------------------
 
-size_t stage2_lds_bytes(int d, int nbt) {
-    return align_up(stage2_head_bytes(d, nbt), 16) + (size_t)kMaxSlice * nbt * 4;
+size_t stage2_lds_bytes(int d, int nbt, int wq) {
+    return align_up(stage2_head_bytes(d, nbt, wq), 16) + (size_t)kMaxSlice * nbt * 4;
+}
+
+int stage2_rows(int d, int wq) {
+    if (wq != 4) return kStage2MaxNB;
+    int r = kStage2MaxNB;   // a power of two, so the launch's row template is r
+    while (r > 1 && !x_in_lds(d, r)) r /= 2;
+    return r;
 }
 
 template <typename K>
@@ -368,53 +515,54 @@ static hipError_t allow_lds(K kernel, size_t bytes) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-template <int NB, int DT, int C>
-static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const void *wg,
-                                  const void *wu, const void *wd, const float *scores, int k_ff,
-                                  uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, Select sel_rule, int act, hipStream_t st) {
-    const size_t lds = stage2_lds_bytes(d, NB);
-    hipError_t e = allow_lds(stage2_kernel<NB, DT, C>, lds);
+template <int NB, int DT, int C, int WQ>
+static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const Stage2Weights &wt,
+                                  const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
+                                  float *ypart, int ystride, int nwg, Select sel_rule, int act,
+                                  hipStream_t st) {
+    if (WQ == 4 && !x_in_lds(d, NB)) return hipErrorInvalidValue;
+    const size_t lds = stage2_lds_bytes(d, NB, WQ);
+    hipError_t e = allow_lds(stage2_kernel<NB, DT, C, WQ>, lds);
     if (e != hipSuccess) return e;
-    stage2_kernel<NB, DT, C><<<nwg, kBlock, lds, st>>>(
-        static_cast<const uint16_t *>(x), nb, d, f, static_cast<const uint16_t *>(wg),
-        static_cast<const uint16_t *>(wu), static_cast<const uint16_t *>(wd), scores, k_ff,
-        mask, scores_copy, ypart, ystride, sel_rule, act);
+    stage2_kernel<NB, DT, C, WQ><<<nwg, kBlock, lds, st>>>(
+        static_cast<const uint16_t *>(x), nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
+        ystride, sel_rule, act);
     return hipGetLastError();
 }
 
-template <int NB, int DT>
-static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const void *wg,
-                                  const void *wu, const void *wd, const float *scores, int k_ff,
-                                  uint8_t *mask, float *scores_copy, float *ypart,
-                                  int ystride, int nwg, Select sel_rule, int act, hipStream_t st) {
+template <int NB, int DT, int WQ>
+static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const Stage2Weights &wt,
+                                  const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
+                                  float *ypart, int ystride, int nwg, Select sel_rule, int act,
+                                  hipStream_t st) {
     // C = score rows per thread of the channel top-k (the dense path has none).
-    if (!scores || f <= 16 * kBlock)
-        return launch_stage2_t<NB, DT, 16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, sel_rule, act, st);
-    if (f <= 32 * kBlock)
-        return launch_stage2_t<NB, DT, 32>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                           scores_copy, ypart, ystride, nwg, sel_rule, act, st);
-    return launch_stage2_t<NB, DT, 64>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,
-                                       scores_copy, ypart, ystride, nwg, sel_rule, act, st);
+#define S2C(C_) launch_stage2_t<NB, DT, C_, WQ>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, st)
+    if (!scores || f <= 16 * kBlock) return S2C(16);
+    if (f <= 32 * kBlock) return S2C(32);
+    return S2C(64);
+#undef S2C
 }
 
-hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const void *wg,
-                         const void *wu, const void *wd, const float *scores, int k_ff,
-                         uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                         int nwg, Select sel_rule, int act, hipStream_t st) {
-#define S2(NB_)                                                                                    \
-    return dtype == kBF16                                                                          \
-               ? launch_stage2_c<NB_, kBF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,    \
-                                             scores_copy, ypart, ystride, nwg, sel_rule, act, st)                 \
-               : launch_stage2_c<NB_, kF16>(x, nb, d, f, wg, wu, wd, scores, k_ff, mask,     \
-                                            scores_copy, ypart, ystride, nwg, sel_rule, act, st)
-    switch (stage2_nb_t(nb)) {
-        case 1: S2(1);
-        case 2: S2(2);
-        case 4: S2(4);
-        default: S2(8);
+hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const Stage2Weights &wt,
+                         const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
+                         float *ypart, int ystride, int nwg, Select sel_rule, int act,
+                         hipStream_t st) {
+    if (nb < 1 || nb > stage2_rows(d, wt.wq)) return hipErrorInvalidValue;
+#define S2(NB_, DT_, WQ_) return launch_stage2_c<NB_, DT_, WQ_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, st)
+#define S2NB(DT_, WQ_)                   \
+    switch (stage2_nb_t(nb)) {           \
+        case 1: S2(1, DT_, WQ_);         \
+        case 2: S2(2, DT_, WQ_);         \
+        case 4: S2(4, DT_, WQ_);         \
+        default: S2(8, DT_, WQ_);        \
     }
+    if (wt.wq == 4) {
+        if (dtype == kBF16) { S2NB(kBF16, 4) }
+        S2NB(kF16, 4)
+    }
+    if (dtype == kBF16) { S2NB(kBF16, 16) }
+    S2NB(kF16, 16)
+#undef S2NB
 #undef S2
 }
 

@@ -47,6 +47,12 @@ class _Proxy(ctypes.Structure):
                 ("bytes", ctypes.c_size_t)]
 
 
+class _W4(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("d_model", ctypes.c_int), ("d_ff", ctypes.c_int),
+                ("group", ctypes.c_int), ("act", ctypes.c_int), ("blob", ctypes.c_void_p),
+                ("bytes", ctypes.c_size_t)]
+
+
 _lib = None
 
 
@@ -81,11 +87,19 @@ def lib() -> ctypes.CDLL:
         L.prox_sparse_stage_name.argtypes = [I]
         L.prox_sparse_stage_name.restype = ctypes.c_char_p
         L.prox_add_rmsnorm.argtypes = [P, P, I, I, I, Z, P, P]
+        QP = ctypes.POINTER(_W4)
+        L.prox_w4_bytes.argtypes = [I, I, I]
+        L.prox_w4_bytes.restype = S
+        L.prox_pack_w4.argtypes = [WP, QP, P]
+        L.prox_unpack_w4.argtypes = [QP, I, P, P, P]
+        L.prox_ffn_dense_w4.argtypes = [QP, P, I, P, P, S, P]
+        L.prox_ffn_sparse_w4.argtypes = [QP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
         L.prox_strerror.argtypes = [I]
         L.prox_strerror.restype = ctypes.c_char_p
         for name in ("prox_pack_proxy", "prox_unpack_proxy", "prox_ffn_dense", "prox_ffn_sparse",
                      "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm",
-                     "prox_reservoir_add", "prox_quantile_threshold", "prox_allocate_sparsity"):
+                     "prox_reservoir_add", "prox_quantile_threshold", "prox_allocate_sparsity",
+                     "prox_pack_w4", "prox_unpack_w4", "prox_ffn_dense_w4", "prox_ffn_sparse_w4"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -294,6 +308,103 @@ def ffn_sparse_tau(w: Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau_s: f
                                      _ptr(in_mask), _ptr(scores), _ptr(counts), _ptr(ws),
                                      ws.numel(), _stream(dev)), "prox_ffn_sparse_tau")
     return y, mask, counts
+
+
+@dataclasses.dataclass
+class W4Weights:
+    """INT4 copy of the three FFN matrices for Stage 2 (W4A16): an opaque
+    device blob in the layout include/prox.h describes."""
+    blob: torch.Tensor
+    dtype: torch.dtype
+    d_model: int
+    d_ff: int
+    group: int
+    act: int = SILU
+
+    def struct(self) -> _W4:
+        _dev_tensor(self.blob, "W4 blob", torch.uint8)
+        return _W4(_TORCH_DT[self.dtype], self.d_model, self.d_ff, self.group, int(self.act),
+                   self.blob.data_ptr(), self.blob.numel())
+
+
+def w4_bytes(d_model: int, d_ff: int, group: int = 128) -> int:
+    return int(lib().prox_w4_bytes(d_model, d_ff, group))
+
+
+def pack_w4(w: Weights, group: int = 128) -> W4Weights:
+    n = w4_bytes(w.d_model, w.d_ff, group)
+    if n == 0:
+        raise ProxError(2, "prox_w4_bytes")
+    q = W4Weights(torch.empty(n, dtype=torch.uint8, device=w.w_gate.device), w.dtype, w.d_model,
+                  w.d_ff, group, w.act)
+    ws, qs = w.struct(), q.struct()
+    _check(lib().prox_pack_w4(ctypes.byref(ws), ctypes.byref(qs), _stream(w.w_gate.device)),
+           "prox_pack_w4")
+    return q
+
+
+def unpack_w4(q: W4Weights, matrix: int):
+    """(codes int8 [d_ff][d_model], scales fp16 bits int16 [d_ff][d_model / group]) of
+    matrix 0 (gate), 1 (up) or 2 (down)."""
+    dev = q.blob.device
+    codes = torch.empty((q.d_ff, q.d_model), dtype=torch.int8, device=dev)
+    scales = torch.empty((q.d_ff, q.d_model // q.group), dtype=torch.int16, device=dev)
+    qs = q.struct()
+    _check(lib().prox_unpack_w4(ctypes.byref(qs), int(matrix), _ptr(codes), _ptr(scales),
+                                _stream(dev)), "prox_unpack_w4")
+    return codes, scales
+
+
+def _as_batch_w4(x: torch.Tensor, q: W4Weights) -> torch.Tensor:
+    x = _dev_tensor(x, "x", q.dtype)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    if x.dim() != 2 or x.shape[1] != q.d_model:
+        raise ValueError("x must be [batch][d_model]")
+    return x
+
+
+def ffn_dense_w4(q: W4Weights, x: torch.Tensor, y: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The dense FFN on the INT4 weights."""
+    x = _as_batch_w4(x, q)
+    B = x.shape[0]
+    y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", q.dtype)
+    ws = new_workspace(q.d_model, q.d_ff, B, x.device) if ws is None else ws
+    qs = q.struct()
+    _check(lib().prox_ffn_dense_w4(ctypes.byref(qs), _ptr(x), B, _ptr(y), _ptr(ws), ws.numel(),
+                                   _stream(x.device)), "prox_ffn_dense_w4")
+    return y
+
+
+def ffn_sparse_w4(q: W4Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int, *,
+                  y: Optional[torch.Tensor] = None, mask: Optional[torch.Tensor] = None,
+                  in_mask: Optional[torch.Tensor] = None, scores: Optional[torch.Tensor] = None,
+                  ws: Optional[torch.Tensor] = None,
+                  events: Optional[Sequence[torch.cuda.Event]] = None):
+    """The sparse decode step with Stage 2 on the INT4 weights.  Returns
+    (y, mask); arguments as ffn_sparse."""
+    x = _as_batch_w4(x, q)
+    B = x.shape[0]
+    dev = x.device
+    y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", q.dtype)
+    mask = (torch.empty(q.d_ff, dtype=torch.uint8, device=dev) if mask is None
+            else _dev_tensor(mask, "mask", torch.uint8))
+    if in_mask is not None:
+        _dev_tensor(in_mask, "in_mask", torch.uint8)
+    if scores is not None:
+        _dev_tensor(scores, "scores", torch.float32)
+    ws = new_workspace(q.d_model, q.d_ff, B, dev) if ws is None else ws
+    arr = None
+    if events is not None:
+        if len(events) != SPARSE_STAGES + 1:
+            raise ValueError(f"need {SPARSE_STAGES + 1} events")
+        arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    qs, pst = q.struct(), p.struct()
+    _check(lib().prox_ffn_sparse_w4(ctypes.byref(qs), ctypes.byref(pst), _ptr(x), B, int(k_in),
+                                    int(k_ff), _ptr(y), _ptr(mask), _ptr(in_mask), _ptr(scores),
+                                    _ptr(ws), ws.numel(), arr, _stream(dev)), "prox_ffn_sparse_w4")
+    return y, mask
 
 
 def effective_sparsity(s1: float, s2: float, alpha: float = 1.0 / 3.0) -> float:

@@ -179,3 +179,48 @@ def test_strerror_and_stage_names():
         assert prox.strerror(s)
     assert prox.stage_names() == ["proxy_gemv_score", "stage2_select_gate_up_down", "reduce_y"]
     assert prox.lib().prox_sparse_stage_name(3) is None
+
+
+def _w4(d=1024, f=3072, dtype=prox.BF16, group=128, act=prox.SILU, blob=FAKE, nbytes=1 << 40):
+    return prox._W4(dtype, d, f, group, act, blob, nbytes)
+
+
+def test_w4_sizes_and_rejects_bad_arguments():
+    d, f = 1024, 3072
+    n = prox.w4_bytes(d, f, 128)
+    assert n >= 3 * f * (d // 2) + 3 * f * (d // 128) * 2
+    assert prox.w4_bytes(d, f, 256) < n                  # fewer scales
+    assert prox.w4_bytes(d, f, 96) == 0                   # group % 128
+    assert prox.w4_bytes(d, f, 384) == 0                  # d % group
+    assert prox.w4_bytes(1000, f, 128) == 0               # d % 128
+    L = prox.lib()
+
+    def dense(q, x=FAKE, B=1, y=FAKE, ws=FAKE, ws_bytes=1 << 40):
+        return L.prox_ffn_dense_w4(ctypes.byref(q), x, B, y, ws, ws_bytes, None)
+
+    def sparse(q, k_in=10, k_ff=10, ws_bytes=1 << 40):
+        p = _proxy()
+        return L.prox_ffn_sparse_w4(ctypes.byref(q), ctypes.byref(p), FAKE, 1, k_in, k_ff, FAKE,
+                                    FAKE, None, None, FAKE, ws_bytes, None, None)
+
+    assert L.prox_ffn_dense_w4(None, FAKE, 1, FAKE, FAKE, 1 << 40, None) == INVALID
+    assert dense(_w4(blob=0)) == INVALID
+    assert dense(_w4(blob=FAKE + 16)) == INVALID          # 256-byte alignment
+    assert dense(_w4(dtype=5)) == INVALID
+    assert dense(_w4(act=7)) == INVALID
+    assert dense(_w4(group=96)) == UNSUPPORTED
+    assert dense(_w4(d=1000)) == UNSUPPORTED
+    assert dense(_w4(nbytes=100)) == WORKSPACE
+    assert dense(_w4(), x=None) == INVALID
+    assert dense(_w4(), B=17) == INVALID
+    assert dense(_w4(), ws_bytes=100) == WORKSPACE
+    assert sparse(_w4(), k_in=0) == INVALID
+    assert sparse(_w4(), k_ff=3073) == INVALID
+    assert sparse(_w4(group=96)) == UNSUPPORTED
+    assert sparse(_w4(), ws_bytes=100) == WORKSPACE
+    q = _w4()
+    assert L.prox_unpack_w4(ctypes.byref(q), 3, FAKE, FAKE, None) == INVALID
+    assert L.prox_unpack_w4(ctypes.byref(q), 0, None, FAKE, None) == INVALID
+    w = _weights()
+    assert L.prox_pack_w4(ctypes.byref(w), ctypes.byref(_w4(d=2048)), None) == INVALID
+    assert L.prox_pack_w4(ctypes.byref(w), ctypes.byref(_w4(dtype=prox.F16)), None) == INVALID

@@ -1,0 +1,124 @@
+"""GPU parity of the INT4 base-weight (W4A16) Stage 2 against the oracle.
+
+Stage 1 is the usual proxy path, so its checks are those of the 16-bit step:
+input top-k bit-exact, the channel mask the exact top-k of the GPU's own
+scores, the scores within the proxy tolerance.  Stage 2 reads the INT4 copy
+of the three matrices (packed bit-exactly like the proxy, checked here), and
+y is compared with the oracle's W4 Stage 2 on the GPU's own mask, to the same
+2e-2 max-abs-rel bar.  Cases cover bf16 and fp16, SiLU and GeGLU, group 256,
+and batches split over several Stage 2 launches (d_model 8192 takes 4 rows
+per launch, 16384 takes 2).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_27591_amd import prox
+from paper_2607_27591_amd import workloads as W
+
+from gpu_cases import SCORE_TOL, Y_TOL, log, make_case, y_rel_err
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "bf16_w4_1024x1600_b1": (W.small_config(d=1024, f=1600, batch=1, seed=71, in_frac=0.4,
+                                            ff_frac=0.3, sigma_w=0.02), prox.SILU),
+    "f16_w4_512x700_b2": (W.small_config(d=512, f=700, batch=2, seed=72, dtype=W.DT_F16,
+                                         ff_frac=0.5), prox.SILU),
+    "bf16_w4_g256_2048x3000_b5": (W.small_config(d=2048, f=3000, batch=5, seed=73, group=256,
+                                                 sigma_w=0.02), prox.SILU),
+    "bf16_w4_geglu_1024x900_b3": (W.small_config(d=1024, f=900, batch=3, seed=74,
+                                                 sigma_w=0.02), prox.GELU),
+    "bf16_w4_8192x640_b7": (W.small_config(d=8192, f=640, batch=7, seed=75, in_frac=0.4,
+                                           sigma_w=0.01), prox.SILU),
+    "bf16_w4_16384x320_b3": (W.small_config(d=16384, f=320, batch=3, seed=76, in_frac=0.3,
+                                            sigma_w=0.01), prox.SILU),
+}
+
+
+@pytest.fixture(scope="module", params=sorted(CASES))
+def case(request):
+    cfg, act = CASES[request.param]
+    cfg = cfg.with_(name=request.param)
+    log(f"[w4 case] {request.param}: d={cfg.d_model} f={cfg.d_ff} B={cfg.batch} "
+        f"group={cfg.group} act={act}")
+    c = make_case(cfg, act=act)
+    q = prox.pack_w4(c.w, cfg.group)
+    w4 = oracle.quantize_w4(c.wl.w_gate, c.wl.w_up, c.wl.w_down, cfg.dtype, cfg.group)
+    yield c, q, w4
+    del c, q
+    torch.cuda.empty_cache()
+
+
+def _run_w4(c, q, x_bits, k_in, k_ff):
+    cfg = c.cfg
+    x = prox.from_bits(np.atleast_2d(x_bits), cfg.dtype)
+    in_mask = torch.empty(cfg.d_model, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(cfg.d_ff, dtype=torch.float32, device="cuda")
+    y, mask = prox.ffn_sparse_w4(q, c.proxy, x, k_in, k_ff, in_mask=in_mask, scores=scores)
+    torch.cuda.synchronize()
+    return prox.to_bits(y), mask.cpu().numpy(), in_mask.cpu().numpy(), scores.cpu().numpy()
+
+
+def test_w4_pack_bit_exact(case):
+    c, q, w4 = case
+    for m, key in enumerate(("g", "u", "d")):
+        codes, scales = prox.unpack_w4(q, m)
+        torch.cuda.synchronize()
+        assert np.array_equal(codes.cpu().numpy(), w4["codes_" + key]), f"codes {key}"
+        assert np.array_equal(scales.cpu().numpy().view(np.uint16), w4["scales_" + key]), \
+            f"scales {key}"
+
+
+def test_w4_sparse_parity(case):
+    c, q, w4 = case
+    cfg = c.cfg
+    for v, x in enumerate(c.wl.x_vectors(2, cfg.batch)):
+        y, mask, in_mask, scores = _run_w4(c, q, x, cfg.k_in, cfg.k_ff)
+        ref = oracle.ffn_sparse_w4(x, cfg.dtype, w4, cfg.k_in, cfg.k_ff, codes_g=c.codes_g,
+                                   scales_g=c.scales_g, codes_u=c.codes_u, scales_u=c.scales_u,
+                                   group=cfg.group, act=c.act)
+        assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"]), f"v{v}: input top-k"
+        gpu_sel = oracle.topk(scores.astype(np.float64), cfg.k_ff)
+        assert np.array_equal(np.flatnonzero(mask), gpu_sel), f"v{v}: select on GPU scores"
+        serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
+        assert serr <= SCORE_TOL * ref["score"].max(), f"v{v}: score err {serr}"
+        _, y_ref = oracle.stage2_w4(x, cfg.dtype, w4, gpu_sel.astype(np.int32), c.act)
+        err = y_rel_err(y, y_ref, cfg.dtype)
+        log(f"    v{v}: y max-abs-rel {err:.2e}")
+        assert err <= Y_TOL, f"v{v}: y err {err}"
+
+
+def test_w4_dense_parity_and_full_keep(case):
+    c, q, w4 = case
+    cfg = c.cfg
+    x_bits = c.wl.x_vectors(1, cfg.batch)[0]
+    x = prox.from_bits(np.atleast_2d(x_bits), cfg.dtype)
+    y_dense = prox.to_bits(prox.ffn_dense_w4(q, x))
+    y_ref = oracle.ffn_dense_w4(x_bits, cfg.dtype, w4, c.act)
+    err = y_rel_err(y_dense, y_ref, cfg.dtype)
+    log(f"    dense W4: y max-abs-rel {err:.2e}")
+    assert err <= Y_TOL
+    # Keeping every input and channel runs the dense channel split: bitwise.
+    y_full, mask, _, _ = _run_w4(c, q, x_bits, cfg.d_model, cfg.d_ff)
+    assert mask.all()
+    assert np.array_equal(y_full, y_dense)
+
+
+def test_w4_c4_full_size():
+    cfg = W.CONFIGS["c4_8192x28672_bf16"]
+    log("[w4 full] c4: generating and packing")
+    c = make_case(cfg)
+    q = prox.pack_w4(c.w, cfg.group)
+    w4 = oracle.quantize_w4(c.wl.w_gate, c.wl.w_up, c.wl.w_down, cfg.dtype, cfg.group)
+    x = c.wl.x_vectors(1, 1)[0]
+    y, mask, in_mask, scores = _run_w4(c, q, x, cfg.k_in, cfg.k_ff)
+    gpu_sel = oracle.topk(scores.astype(np.float64), cfg.k_ff)
+    assert np.array_equal(np.flatnonzero(mask), gpu_sel)
+    _, y_ref = oracle.stage2_w4(x, cfg.dtype, w4, gpu_sel.astype(np.int32))
+    err = y_rel_err(y, y_ref, cfg.dtype)
+    log(f"    c4 W4: y max-abs-rel {err:.2e}")
+    assert err <= Y_TOL
+    del c, q
+    torch.cuda.empty_cache()

@@ -48,6 +48,7 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-tau", action="store_true", help="skip the threshold-mode leg")
+    ap.add_argument("--no-w4", action="store_true", help="skip the INT4 base-weight (W4A16) leg")
     ap.add_argument("--alpha", action="store_true",
                     help="measure the proxy-cost ratio alpha (quantised over 16-bit proxy)")
     ap.add_argument("--calib-tokens", type=int, default=32,
@@ -73,6 +74,17 @@ def algorithmic_bytes(cfg, B, k_in, k_ff):
         "down_rows": k_ff * d * e,
         "y": B * d * e,
     }
+
+
+def w4_bytes(cfg, B, k_in, k_ff):
+    """Bytes of the sparse step with Stage 2 on INT4 base weights: Stage 1 as
+    algorithmic_bytes, then the kept channels' codes (d / 2 bytes per row)
+    and scales (d / group fp16 per row) of the three matrices."""
+    ab = algorithmic_bytes(cfg, B, k_in, k_ff)
+    d, ng = cfg.d_model, cfg.d_model // cfg.group
+    row = d // 2 + ng * 2
+    return {"x": ab["x"], "proxy_codes": ab["proxy_codes"], "proxy_scales": ab["proxy_scales"],
+            "gate_up_rows": 2 * k_ff * row, "down_rows": k_ff * row, "y": ab["y"]}
 
 
 def dense_bytes(cfg, B):
@@ -250,6 +262,10 @@ def main():
                 "frac": round(s2_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": s2_bytes, "avg_launch_us": round(s2_us, 2)}
 
+    w4 = None
+    if not args.no_w4:
+        w4 = w4_leg(args, cfg, w, proxy, xs, n_x, B, ws, y, mask, k_in, k_ff, timed, prox)
+
     tau = None
     if not args.no_tau:
         tau = threshold_leg(args, cfg, wl, w, proxy, xs, n_x, B, ws, y, mask, flush, sink,
@@ -295,8 +311,49 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "threshold_mode": tau,
+        "w4a16": w4,
     }
     print(json.dumps(out), flush=True)
+
+
+def w4_leg(args, cfg, w, proxy, xs, n_x, B, ws, y, mask, k_in, k_ff, timed, prox):
+    """The same workload with Stage 2 on INT4 base weights (W4A16, the
+    combination Sec. 5.1 leaves to future work), and the dense FFN on the
+    same INT4 weights as its baseline; same cold protocol and decode vectors."""
+    q = prox.pack_w4(w, cfg.group)
+
+    def sparse(i, events=None):
+        prox.ffn_sparse_w4(q, proxy, xs[i % n_x], k_in, k_ff, y=y, mask=mask, ws=ws,
+                           events=events)
+
+    def dense(i):
+        prox.ffn_dense_w4(q, xs[i % n_x], y=y, ws=ws)
+
+    for i in range(args.warmup):
+        sparse(i)
+        dense(i)
+    us, _ = timed(sparse, args.steps, cold=not args.warm)
+    _, st = timed(sparse, args.steps, cold=not args.warm, staged=True)
+    dus, _ = timed(dense, args.steps, cold=not args.warm)
+    del q
+    names = prox.stage_names()
+    stage_us = {n: statistics.mean(r[s] for r in st) for s, n in enumerate(names)}
+    ab = w4_bytes(cfg, B, k_in, k_ff)
+    mean, med, dmed = statistics.mean(us), statistics.median(us), statistics.median(dus)
+    d, f, ng = cfg.d_model, cfg.d_ff, cfg.d_model // cfg.group
+    dense_b = 3 * f * (d // 2 + ng * 2) + 2 * B * d * 2
+    s2_bytes = ab["gate_up_rows"] + ab["down_rows"] + 4 * f
+    s2_us = stage_us["stage2_select_gate_up_down"]
+    return {"weights": f"int4 group {cfg.group} fp16 scales, all three matrices",
+            "us_per_call": {"mean": round(mean, 2), "median": round(med, 2),
+                            "p10": round(pct(us, 0.1), 2), "p90": round(pct(us, 0.9), 2)},
+            "algorithmic_bytes": sum(ab.values()),
+            "algorithmic_gbs": round(sum(ab.values()) / (mean * 1e-6) / 1e9, 1),
+            "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
+            "stage2_gbs": round(s2_bytes / (s2_us * 1e-6) / 1e9, 1),
+            "dense_w4_us_per_call": round(dmed, 2),
+            "dense_w4_gbs": round(dense_b / (dmed * 1e-6) / 1e9, 1),
+            "speedup_vs_dense_w4": round(dmed / med, 3)}
 
 
 def threshold_leg(args, cfg, wl, w, proxy, xs, n_x, B, ws, y, mask, flush, sink, k_in, k_ff,

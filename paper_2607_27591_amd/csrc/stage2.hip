@@ -25,10 +25,10 @@ constexpr int kMaxSlice = (kMaxDFF + kStage2MaxWGs - 1) / kStage2MaxWGs;   // ch
 constexpr int kMaxParts = 8;
 
 // d is cut into Q parts for the gate/up units (each part >= 2048 columns of
-// 16-bit weights, >= 4096 of INT4 codes: at least two 16-byte loads per lane).
+// 16-bit weights, >= 8192 of INT4 codes: up to four 16-byte loads per lane).
 __host__ __device__ inline int gateup_parts(int d, int nbt, int wq) {
     if (nbt > 2) return 1;
-    int q = d / (wq == 4 ? 4096 : 2048);
+    int q = d / (wq == 4 ? 8192 : 2048);
     return q < 1 ? 1 : (q > kMaxParts ? kMaxParts : q);
 }
 
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         const int nv4 = d / 32;
         const int qv = nv4 / Q;
         const uint4 *xs4 = reinterpret_cast<const uint4 *>(xs);
-        constexpr int U = 2;
+        constexpr int U = NB <= 2 ? 4 : 2;   // vectors in flight per lane and matrix
         for (int unit = wid; unit < n * Q; unit += kMaxBlockWaves) {
             const int t = unit / Q, q = unit % Q;
             const int j = sm.list[t];
@@ -331,14 +331,20 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
             for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
         if constexpr (WQ == 4) {
             // 8 columns per thread: one 32-bit code word and the scale of
-            // their group per channel row.
+            // their group per channel row.  The codes n = q + 8 are split into
+            // bytes and converted one byte each; sum_j s_j sigma_j (n - 8) is
+            // taken as sum_j s_j sigma_j n minus 8 sum_j s_j sigma_j, once.
             const int ng = d / wt.group;
-            if (active) {
-                for (int t0 = gi; t0 < n; t0 += G * UD) {
-                    uint32_t cw[UD];
-                    uint16_t sb[UD];
+            constexpr int UD4 = NB <= 2 ? 16 : 8;   // rows in flight: 4 bytes each
+            float ssum[NB];
 #pragma unroll
-                    for (int u = 0; u < UD; ++u) {
+            for (int b = 0; b < NB; ++b) ssum[b] = 0.0f;
+            if (active) {
+                for (int t0 = gi; t0 < n; t0 += G * UD4) {
+                    uint32_t cw[UD4];
+                    uint16_t sb[UD4];
+#pragma unroll
+                    for (int u = 0; u < UD4; ++u) {
                         const int t = t0 + u * G;
                         if (t < n) {
                             const int j = sm.list[t];
@@ -348,16 +354,22 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                         }
                     }
 #pragma unroll
-                    for (int u = 0; u < UD; ++u) {
+                    for (int u = 0; u < UD4; ++u) {
                         const int t = t0 + u * G;
                         if (t < n) {
                             const float sc = f16_bits_to_float(sb[u]);
+                            const uint32_t lo = cw[u] & 0x0F0F0F0Fu;          // columns 0, 2, 4, 6
+                            const uint32_t hi = (cw[u] >> 4) & 0x0F0F0F0Fu;   // columns 1, 3, 5, 7
                             float wf[8];
 #pragma unroll
-                            for (int e = 0; e < 8; ++e) wf[e] = (float)(int)((cw[u] >> (4 * e)) & 15u) - 8.0f;
+                            for (int k = 0; k < 4; ++k) {
+                                wf[2 * k] = (float)((lo >> (8 * k)) & 0xFFu);
+                                wf[2 * k + 1] = (float)((hi >> (8 * k)) & 0xFFu);
+                            }
 #pragma unroll
                             for (int b = 0; b < NB; ++b) {
                                 const float sv = s_sh[t * NB + b] * sc;
+                                ssum[b] += sv;
 #pragma unroll
                                 for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
                             }
@@ -365,6 +377,10 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                     }
                 }
             }
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(-8.0f, ssum[b], acc[b][e]);
         } else if (active) {
             for (int t0 = gi; t0 < n; t0 += G * UD) {
                 uint4 wv[UD];

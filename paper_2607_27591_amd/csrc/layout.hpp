@@ -11,7 +11,6 @@ constexpr int kF16 = 0;
 constexpr int kBF16 = 1;
 constexpr int kMaxDModel = 16384;   // multiple of 128
 constexpr int kMaxDFF = 65536;
-constexpr int kMaxBatch = 16;
 constexpr int kBlock = 1024;        // threads per workgroup of the main kernels
 constexpr int kMaxBlockWaves = kBlock / 64;
 

@@ -75,11 +75,12 @@ def test_sizes():
     assert prox.proxy_bytes(1024, 3072, prox.INT4, 512 * 3) == 0   # d % group
     assert prox.proxy_bytes(1024, 3072, 7, 128) == 0               # fmt
     assert prox.workspace_bytes(4096, 12288, 1) > 0
-    assert prox.workspace_bytes(4096, 12288, 17) == 0
+    assert prox.workspace_bytes(4096, 12288, 65) == 0
     assert prox.workspace_bytes(4096, 12288, 0) == 0
     assert prox.workspace_bytes(32768, 12288, 1) == 0
     assert prox.workspace_bytes(4096, 65537, 1) == 0
     assert prox.workspace_bytes(4096, 12288, 16) > prox.workspace_bytes(4096, 12288, 1)
+    assert prox.workspace_bytes(4096, 12288, 64) > prox.workspace_bytes(4096, 12288, 16)
 
 
 def test_stage1_kernel_selection():
@@ -98,7 +99,8 @@ def test_stage1_kernel_selection():
     assert rows(4096, prox.INT8, 128, 16, 2048) == 0
     assert rows(4096, prox.NONE, 4096, 16, 2048) == 0
     assert rows(4096, prox.INT4, 96, 16, 2048) == 0        # group % 128
-    assert rows(4096, prox.INT4, 128, 17, 2048) == 0       # batch
+    assert rows(4096, prox.INT4, 128, 65, 2048) == 0       # batch
+    assert rows(4096, prox.INT4, 128, 64, 2048) == 16
     assert rows(4096, prox.INT4, 128, 16, 0) == 0          # k_in
     assert rows(4096, prox.INT4, 128, 16, 4097) == 0
 
@@ -110,7 +112,7 @@ def test_sparse_rejects_bad_arguments():
     assert _sparse(k_ff=0) == INVALID
     assert _sparse(k_ff=3073) == INVALID
     assert _sparse(B=0) == INVALID
-    assert _sparse(B=17) == INVALID
+    assert _sparse(B=65) == INVALID
     assert _sparse(x=None) == INVALID
     assert _sparse(y=None) == INVALID
     assert _sparse(mask=None) == INVALID
@@ -149,7 +151,7 @@ def test_sparse_tau_rejects_bad_arguments():
     assert call(tau_s=nan) == INVALID
     assert call(counts=MISALIGNED) == INVALID
     assert call(B=0) == INVALID
-    assert call(B=17) == INVALID
+    assert call(B=65) == INVALID
     assert call(mask=None) == INVALID
     assert call(ws_bytes=10) == WORKSPACE
     assert call(tau_x=float("inf"), ws_bytes=10) == WORKSPACE   # +inf is a valid threshold
@@ -212,7 +214,7 @@ def test_w4_sizes_and_rejects_bad_arguments():
     assert dense(_w4(d=1000)) == UNSUPPORTED
     assert dense(_w4(nbytes=100)) == WORKSPACE
     assert dense(_w4(), x=None) == INVALID
-    assert dense(_w4(), B=17) == INVALID
+    assert dense(_w4(), B=65) == INVALID
     assert dense(_w4(), ws_bytes=100) == WORKSPACE
     assert sparse(_w4(), k_in=0) == INVALID
     assert sparse(_w4(), k_ff=3073) == INVALID

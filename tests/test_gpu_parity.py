@@ -34,6 +34,13 @@ SMALL = {
     "f16_i4_768x900_b7": W.small_config(d=768, f=900, batch=7, seed=13, dtype=W.DT_F16),
     "bf16_i4_4096x1500_b12": W.small_config(d=4096, f=1500, batch=12, seed=14, in_frac=0.7,
                                             sigma_w=0.02),
+    # Batches past one launch's rows: 40 rows on the matrix cores (16 + 16 + 8
+    # per Stage 1 launch, five 8-row Stage 2 launches), and 20 INT8 rows on the
+    # dot-product kernel (five 4-row Stage 1 launches).
+    "bf16_i4_1024x1600_b40": W.small_config(d=1024, f=1600, batch=40, seed=16, in_frac=0.4,
+                                            sigma_w=0.02),
+    "f16_i8_512x700_b20": W.small_config(d=512, f=700, batch=20, seed=17, dtype=W.DT_F16,
+                                         qbits=8, group=512, ff_frac=0.5),
     # d_model 16384 on the matrix cores: 16 input rows per thread, 8 batch
     # rows per launch.
     "bf16_i4_16384x320_b6": W.small_config(d=16384, f=320, batch=6, seed=15, in_frac=0.3,

@@ -7,7 +7,7 @@ of the three matrices (packed bit-exactly like the proxy, checked here), and
 y is compared with the oracle's W4 Stage 2 on the GPU's own mask, to the same
 2e-2 max-abs-rel bar.  Cases cover bf16 and fp16, SiLU and GeGLU, group 256,
 and batches split over several Stage 2 launches (d_model 8192 takes 4 rows
-per launch, 16384 takes 2).
+per launch, 16384 takes 2; 24 rows at 8192 take six).
 """
 import numpy as np
 import pytest
@@ -32,6 +32,8 @@ CASES = {
                                                  sigma_w=0.02), prox.GELU),
     "bf16_w4_8192x640_b7": (W.small_config(d=8192, f=640, batch=7, seed=75, in_frac=0.4,
                                            sigma_w=0.01), prox.SILU),
+    "bf16_w4_8192x512_b24": (W.small_config(d=8192, f=512, batch=24, seed=77, in_frac=0.4,
+                                            sigma_w=0.01), prox.SILU),
     "bf16_w4_16384x320_b3": (W.small_config(d=16384, f=320, batch=3, seed=76, in_frac=0.3,
                                             sigma_w=0.01), prox.SILU),
 }

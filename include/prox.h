@@ -262,6 +262,13 @@ prox_status prox_ffn_sparse_w4(const prox_w4_weights *q, const prox_proxy *p, co
                                uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
                                hipEvent_t *events, hipStream_t stream);
 
+/* The threshold-mode step of prox_ffn_sparse_tau with Stage 2 on the INT4
+ * weights.  Arguments as prox_ffn_sparse_tau, with q in place of w. */
+prox_status prox_ffn_sparse_tau_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
+                                   int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
+                                   uint8_t *in_mask, float *scores, int32_t *counts, void *ws,
+                                   size_t ws_bytes, hipStream_t stream);
+
 /*
  * Threshold calibration (App. A.7), host code only (no HIP calls; all
  * pointers are host memory).  Offline, a layer's thresholds come from

@@ -329,6 +329,16 @@ prox_status prox_ffn_dense_w4(const prox_w4_weights *q, const void *x, int batch
     return dense_impl(model_of(q), x, batch, y, ws, ws_bytes, stream);
 }
 
+prox_status prox_ffn_sparse_tau_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
+                                   int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
+                                   uint8_t *in_mask, float *scores, int32_t *counts, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+    prox_status st = check_w4(q);
+    if (st != PROX_OK) return st;
+    return sparse_impl(model_of(q), p, x, batch, 0, 0, Rules{1, tau_x, tau_s, counts}, y, mask,
+                       in_mask, scores, ws, ws_bytes, nullptr, stream);
+}
+
 prox_status prox_ffn_sparse_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
                                int batch, int k_in, int k_ff, void *y, uint8_t *mask,
                                uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,

@@ -94,12 +94,14 @@ def lib() -> ctypes.CDLL:
         L.prox_unpack_w4.argtypes = [QP, I, P, P, P]
         L.prox_ffn_dense_w4.argtypes = [QP, P, I, P, P, S, P]
         L.prox_ffn_sparse_w4.argtypes = [QP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
+        L.prox_ffn_sparse_tau_w4.argtypes = [QP, PP, P, I, Z, Z, P, P, P, P, P, P, S, P]
         L.prox_strerror.argtypes = [I]
         L.prox_strerror.restype = ctypes.c_char_p
         for name in ("prox_pack_proxy", "prox_unpack_proxy", "prox_ffn_dense", "prox_ffn_sparse",
                      "prox_ffn_sparse_staged", "prox_ffn_sparse_tau", "prox_add_rmsnorm",
                      "prox_reservoir_add", "prox_quantile_threshold", "prox_allocate_sparsity",
-                     "prox_pack_w4", "prox_unpack_w4", "prox_ffn_dense_w4", "prox_ffn_sparse_w4"):
+                     "prox_pack_w4", "prox_unpack_w4", "prox_ffn_dense_w4", "prox_ffn_sparse_w4",
+                     "prox_ffn_sparse_tau_w4"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -405,6 +407,34 @@ def ffn_sparse_w4(q: W4Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int,
                                     int(k_ff), _ptr(y), _ptr(mask), _ptr(in_mask), _ptr(scores),
                                     _ptr(ws), ws.numel(), arr, _stream(dev)), "prox_ffn_sparse_w4")
     return y, mask
+
+
+def ffn_sparse_tau_w4(q: W4Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau_s: float, *,
+                      y: Optional[torch.Tensor] = None, mask: Optional[torch.Tensor] = None,
+                      in_mask: Optional[torch.Tensor] = None,
+                      scores: Optional[torch.Tensor] = None,
+                      counts: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """Threshold-mode step with Stage 2 on the INT4 weights.  Returns
+    (y, mask, counts) like ffn_sparse_tau."""
+    x = _as_batch_w4(x, q)
+    B = x.shape[0]
+    dev = x.device
+    y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", q.dtype)
+    mask = (torch.empty(q.d_ff, dtype=torch.uint8, device=dev) if mask is None
+            else _dev_tensor(mask, "mask", torch.uint8))
+    counts = (torch.empty(2, dtype=torch.int32, device=dev) if counts is None
+              else _dev_tensor(counts, "counts", torch.int32))
+    if in_mask is not None:
+        _dev_tensor(in_mask, "in_mask", torch.uint8)
+    if scores is not None:
+        _dev_tensor(scores, "scores", torch.float32)
+    ws = new_workspace(q.d_model, q.d_ff, B, dev) if ws is None else ws
+    qs, pst = q.struct(), p.struct()
+    _check(lib().prox_ffn_sparse_tau_w4(ctypes.byref(qs), ctypes.byref(pst), _ptr(x), B,
+                                        float(tau_x), float(tau_s), _ptr(y), _ptr(mask),
+                                        _ptr(in_mask), _ptr(scores), _ptr(counts), _ptr(ws),
+                                        ws.numel(), _stream(dev)), "prox_ffn_sparse_tau_w4")
+    return y, mask, counts
 
 
 def effective_sparsity(s1: float, s2: float, alpha: float = 1.0 / 3.0) -> float:

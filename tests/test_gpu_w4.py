@@ -18,6 +18,7 @@ from paper_2607_27591_amd import prox
 from paper_2607_27591_amd import workloads as W
 
 from gpu_cases import SCORE_TOL, Y_TOL, log, make_case, y_rel_err
+from test_gpu_threshold import quantile_taus
 
 pytestmark = pytest.mark.gpu
 
@@ -106,6 +107,38 @@ def test_w4_dense_parity_and_full_keep(case):
     y_full, mask, _, _ = _run_w4(c, q, x_bits, cfg.d_model, cfg.d_ff)
     assert mask.all()
     assert np.array_equal(y_full, y_dense)
+
+
+def test_w4_threshold_mode(case):
+    # Thresholds in place of counts (prox_ffn_sparse_tau_w4): the masks follow
+    # the rule exactly on the GPU's own values, y is the oracle's W4 Stage 2 on
+    # the GPU's mask.
+    c, q, w4 = case
+    cfg = c.cfg
+    x_bits = c.wl.x_vectors(1, cfg.batch)[0]
+    tau_x, tau_s = quantile_taus(c, x_bits)
+    x = prox.from_bits(np.atleast_2d(x_bits), cfg.dtype)
+    in_mask = torch.empty(cfg.d_model, dtype=torch.uint8, device="cuda")
+    scores = torch.empty(cfg.d_ff, dtype=torch.float32, device="cuda")
+    y, mask, counts = prox.ffn_sparse_tau_w4(q, c.proxy, x, tau_x, tau_s, in_mask=in_mask,
+                                             scores=scores)
+    torch.cuda.synchronize()
+    y, mask, counts = prox.to_bits(y), mask.cpu().numpy(), counts.cpu().numpy().tolist()
+    in_mask, scores = in_mask.cpu().numpy(), scores.cpu().numpy()
+    ref = oracle.ffn_sparse_tau(x_bits, cfg.dtype, c.wl.w_gate, c.wl.w_up, c.wl.w_down, tau_x,
+                                tau_s, codes_g=c.codes_g, scales_g=c.scales_g, codes_u=c.codes_u,
+                                scales_u=c.scales_u, group=cfg.group, act=c.act)
+    assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"])
+    assert counts[0] == ref["k_in"]
+    gpu_sel = np.flatnonzero(scores >= np.float32(tau_s))
+    assert np.array_equal(np.flatnonzero(mask), gpu_sel)
+    assert counts[1] == gpu_sel.size
+    serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
+    assert serr <= SCORE_TOL * ref["score"].max()
+    _, y_ref = oracle.stage2_w4(x_bits, cfg.dtype, w4, gpu_sel.astype(np.int32), c.act)
+    err = y_rel_err(y, y_ref, cfg.dtype)
+    log(f"    tau W4: k_in {counts[0]} k_ff {counts[1]} y max-abs-rel {err:.2e}")
+    assert err <= Y_TOL
 
 
 def test_w4_c4_full_size():

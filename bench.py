@@ -125,7 +125,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
-              "(this build runs the sparse decode step on one GPU)",
+              "(libprox runs the sparse decode step on a single GPU; sharding along d_ff "
+              "is a design note, not code)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -94,17 +94,24 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
                                                     align_up((size_t)NX * cap * 2, 16));
 
     // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
+    // x is read XQ rows at a time so their loads are in flight together.
+    constexpr int XQ = C <= 8 ? 4 : 2;
     uint32_t key[C];
 #pragma unroll
     for (int r = 0; r < C; ++r) key[r] = 0u;
-    for (int b = 0; b < B_all; ++b) {
-        const uint16_t *xb = x_all + (size_t)b * d;
-        uint32_t raw[C];
+    for (int b0 = 0; b0 < B_all; b0 += XQ) {
+        uint32_t raw[XQ][C];
 #pragma unroll
-        for (int r = 0; r < C; ++r) raw[r] = xb[min(r * kBlock + tid, d - 1)];
+        for (int q = 0; q < XQ; ++q) {
+            const uint16_t *xb = x_all + (size_t)min(b0 + q, B_all - 1) * d;
 #pragma unroll
-        for (int r = 0; r < C; ++r)
-            if (r * kBlock + tid < d) key[r] = max(key[r], raw[r] & 0x7FFFu);
+            for (int r = 0; r < C; ++r) raw[q][r] = xb[min(r * kBlock + tid, d - 1)];
+        }
+#pragma unroll
+        for (int q = 0; q < XQ; ++q)
+#pragma unroll
+            for (int r = 0; r < C; ++r)
+                if (r * kBlock + tid < d) key[r] = max(key[r], raw[q][r] & 0x7FFFu);
     }
     uint64_t sel = 0;
     if (sel_rule.tau_mode) {
@@ -153,14 +160,20 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     }
     // Only the nb real batch rows are stored: the stream feeds zeros for the
     // others.
-    for (int b = 0; b < nb; ++b) {
-        const uint16_t *xb = x_all + (size_t)(row0 + b) * d;
-        uint16_t xv[C];
+    for (int b0 = 0; b0 < nb; b0 += XQ) {
+        uint16_t xv[XQ][C];
 #pragma unroll
-        for (int r = 0; r < C; ++r) xv[r] = xb[min(r * kBlock + tid, d - 1)];
+        for (int q = 0; q < XQ; ++q) {
+            const uint16_t *xb = x_all + (size_t)(row0 + min(b0 + q, nb - 1)) * d;
 #pragma unroll
-        for (int r = 0; r < C; ++r)
-            if (pos[r] >= 0) xs_sh[b * cap + pos[r]] = xv[r];
+            for (int r = 0; r < C; ++r) xv[q][r] = xb[min(r * kBlock + tid, d - 1)];
+        }
+#pragma unroll
+        for (int q = 0; q < XQ; ++q)
+            if (b0 + q < nb)
+#pragma unroll
+                for (int r = 0; r < C; ++r)
+                    if (pos[r] >= 0) xs_sh[(b0 + q) * cap + pos[r]] = xv[q][r];
     }
     __syncthreads();   // the kept rows are in place: pads copy the group's last one
     for (int g = tid; g < ng; g += kBlock) {

@@ -82,6 +82,7 @@ prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_E
 
 struct Ws {
     float *scores, *ypart;
+    int32_t *klist;
 };
 
 Ws carve(void *ws, int d, int f, int batch) {
@@ -90,6 +91,7 @@ Ws carve(void *ws, int d, int f, int batch) {
     Ws w;
     w.scores = reinterpret_cast<float *>(b + L.scores);
     w.ypart = reinterpret_cast<float *>(b + L.ypart);
+    w.klist = reinterpret_cast<int32_t *>(b + L.klist);
     return w;
 }
 
@@ -110,10 +112,13 @@ prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff
     const int rows = stage2_rows(d, m.s2.wq);
     for (int c0 = 0; c0 < batch; c0 += rows) {
         const int nb = batch - c0 < rows ? batch - c0 : rows;
+        const int list_mode = !scores || rows >= batch ? kListNone
+                              : c0 == 0             ? kListWrite
+                                                    : kListRead;
         PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
                                c0 == 0 ? scores_copy : nullptr, W.ypart + (size_t)c0 * d, ystride,
                                nwg, c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, m.act,
-                               stream));
+                               W.klist, list_mode, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
     PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));

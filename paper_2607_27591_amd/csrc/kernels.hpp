@@ -50,10 +50,15 @@ int stage2_rows(int d, int wq);
 // NULL runs the dense FFN over all f channels; otherwise the top k_ff scores,
 // or the threshold rule of sel, pick the channels.  Partial y rows go to
 // ypart[(w * ystride + b) * d + c] for workgroup w < nwg.
+// A batch split over several Stage 2 launches selects once: the first launch
+// (kListWrite) also writes the kept channels in ascending order to klist[0..n)
+// and their count n to klist[f]; the later ones (kListRead) take their slice
+// from it.  kListNone: a single launch, klist unused.
+enum KeptList { kListNone = 0, kListWrite = 1, kListRead = 2 };
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const Stage2Weights &w,
                          const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                          float *ypart, int ystride, int nwg, Select sel, int act,
-                         hipStream_t stream);
+                         int32_t *klist, int klist_mode, hipStream_t stream);
 // INT4 base weights: quantise W_gate, W_up, W_down (channel-major [f][d]) into
 // a W4Layout blob, and the inverse view of matrix m (0 gate, 1 up, 2 down).
 hipError_t launch_pack_w4(int dtype, const void *wg, const void *wu, const void *wd, int d, int f,

@@ -133,11 +133,12 @@ struct Select {
 // scores: the proxy scores (fp32, f padded to 128); ypart: per-workgroup
 // partial y rows of Stage 2.
 struct WsLayout {
-    size_t scores, ypart, total;
+    size_t scores, klist, ypart, total;
     __host__ __device__ WsLayout(int d, int f, int batch) {
         const int f_pad = (f + 127) / 128 * 128;
         size_t o = 0;
         scores = o; o = align_up(o + (size_t)f_pad * 4, 256);
+        klist = o; o = align_up(o + (size_t)(f + 1) * 4, 256);   // kept channels, then their count
         ypart = o; o = align_up(o + (size_t)kStage2MaxWGs * ypart_rows(batch) * d * 4, 256);
         total = o;
     }

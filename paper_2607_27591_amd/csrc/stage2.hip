@@ -65,7 +65,8 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const float *__restrict__ scores,   // NULL: dense FFN over all f channels
     int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
     float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
-    Select sel_rule, int act) {                     // act: gate activation
+    Select sel_rule, int act,                       // act: gate activation
+    int32_t *__restrict__ klist, int klist_mode) {  // kept-channel list, KeptList mode
     static_assert(WQ == 16 || WQ == 4, "16-bit or INT4 weights");
     const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
     const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
@@ -85,7 +86,19 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
 
     // ---- prologue: this workgroup's slice of the kept channels ----
-    if (sparse) {
+    if (sparse && klist_mode == kListRead) {
+        // A launch for the same call already selected: its list gives the
+        // same slice as ranking again would.
+        n_ch = klist[f];
+        if (sel_rule.tau_mode) {
+            const int nwg_k = min(nwg, stage2_wgs(n_ch));
+            p0 = w < nwg_k ? (int)((long long)w * n_ch / nwg_k) : n_ch;
+            p1 = w < nwg_k ? (int)((long long)(w + 1) * n_ch / nwg_k) : n_ch;
+            n = p1 - p0;
+        }
+        for (int t = tid; t < n; t += kBlock) sm.list[t] = klist[p0 + t];
+        __syncthreads();
+    } else if (sparse) {
         // Item r of thread t is channel r * kBlock + t (coalesced loads).
         // Scores are |s~| >= 0, so their IEEE bit patterns order like the
         // values.  Clamped indices, masked later: all loads are in flight at once.
@@ -116,7 +129,11 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         }
         // This workgroup's slice of positions and its chunk of the mask,
         // straight from the order tables.
-        for (int t = tid; t < n; t += kBlock) sm.list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
+        for (int t = tid; t < n; t += kBlock) {
+            sm.list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
+            if (klist_mode == kListWrite) klist[p0 + t] = sm.list[t];
+        }
+        if (klist_mode == kListWrite && w == 0 && tid == 0) klist[f] = n_ch;
         const int mchunk = (f + nwg - 1) / nwg;   // mask entries written by this workgroup
         const int m_lo = w * mchunk, m_hi = min(m_lo + mchunk, f);
         for (int i = m_lo + tid; i < m_hi; i += kBlock) {
@@ -535,14 +552,14 @@ template <int NB, int DT, int C, int WQ>
 static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const Stage2Weights &wt,
                                   const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                                   float *ypart, int ystride, int nwg, Select sel_rule, int act,
-                                  hipStream_t st) {
+                                  int32_t *klist, int klist_mode, hipStream_t st) {
     if (WQ == 4 && !x_in_lds(d, NB)) return hipErrorInvalidValue;
     const size_t lds = stage2_lds_bytes(d, NB, WQ);
     hipError_t e = allow_lds(stage2_kernel<NB, DT, C, WQ>, lds);
     if (e != hipSuccess) return e;
     stage2_kernel<NB, DT, C, WQ><<<nwg, kBlock, lds, st>>>(
         static_cast<const uint16_t *>(x), nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
-        ystride, sel_rule, act);
+        ystride, sel_rule, act, klist, klist_mode);
     return hipGetLastError();
 }
 
@@ -550,9 +567,9 @@ template <int NB, int DT, int WQ>
 static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const Stage2Weights &wt,
                                   const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                                   float *ypart, int ystride, int nwg, Select sel_rule, int act,
-                                  hipStream_t st) {
+                                  int32_t *klist, int klist_mode, hipStream_t st) {
     // C = score rows per thread of the channel top-k (the dense path has none).
-#define S2C(C_) launch_stage2_t<NB, DT, C_, WQ>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, st)
+#define S2C(C_) launch_stage2_t<NB, DT, C_, WQ>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, klist, klist_mode, st)
     if (!scores || f <= 16 * kBlock) return S2C(16);
     if (f <= 32 * kBlock) return S2C(32);
     return S2C(64);
@@ -562,9 +579,10 @@ static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const Sta
 hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const Stage2Weights &wt,
                          const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                          float *ypart, int ystride, int nwg, Select sel_rule, int act,
-                         hipStream_t st) {
+                         int32_t *klist, int klist_mode, hipStream_t st) {
     if (nb < 1 || nb > stage2_rows(d, wt.wq)) return hipErrorInvalidValue;
-#define S2(NB_, DT_, WQ_) return launch_stage2_c<NB_, DT_, WQ_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, st)
+    if (klist_mode != kListNone && (!scores || !klist)) return hipErrorInvalidValue;
+#define S2(NB_, DT_, WQ_) return launch_stage2_c<NB_, DT_, WQ_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, klist, klist_mode, st)
 #define S2NB(DT_, WQ_)                   \
     switch (stage2_nb_t(nb)) {           \
         case 1: S2(1, DT_, WQ_);         \

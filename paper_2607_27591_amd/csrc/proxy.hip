@@ -434,11 +434,14 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
     return hipGetLastError();
 }
 
-// C = input rows per thread of the input top-k: 8 up to d = 8192, else 16.
+// C = input rows per thread of the input top-k: 4 up to d = 4096, 8 up to
+// 8192, else 16.
 template <int NB, int DT, int QB, int T>
 static hipError_t launch_proxy_c(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                  int group, int k_in, const void *blob,
                                  uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
+    if (d <= 4 * kBlock)
+        return launch_proxy_t<NB, DT, QB, T, 4>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
     if (d <= 8 * kBlock)
         return launch_proxy_t<NB, DT, QB, T, 8>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
     return launch_proxy_t<NB, DT, QB, T, 16>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);

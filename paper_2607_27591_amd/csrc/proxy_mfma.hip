@@ -337,6 +337,7 @@ static hipError_t launch_mfma_c(const void *x_all, int B_all, int row0, int nb, 
                                 float *scores, int accumulate, Select sel, int act, hipStream_t s) {
     const int nx = proxy_mfma_rows(d, group, k_in);
 #define MF(C_, NX_) launch_mfma_t<DT, T, C_, NX_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
+    if (d <= 4 * kBlock) return nx == 16 ? MF(4, 16) : MF(4, 8);
     if (d <= 8 * kBlock) return nx == 16 ? MF(8, 16) : MF(8, 8);
     return nx == 16 ? MF(16, 16) : MF(16, 8);
 #undef MF

@@ -570,13 +570,15 @@ static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const Sta
                                   int32_t *klist, int klist_mode, hipStream_t st) {
     // C = score rows per thread of the channel top-k (the dense path has none).
 #define S2C(C_) launch_stage2_t<NB, DT, C_, WQ>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, klist, klist_mode, st)
-    // Fewer score rows per thread for small d_ff (not for eight rows of INT4
-    // weights, whose registers are full).
+    // As few score rows per thread as d_ff needs (below 16 not for eight rows
+    // of INT4 weights, whose registers are full).
     if constexpr (WQ == 16 || NB <= 4) {
         if (scores && f <= 4 * kBlock) return S2C(4);
         if (scores && f <= 8 * kBlock) return S2C(8);
+        if (scores && f <= 12 * kBlock) return S2C(12);
     }
     if (!scores || f <= 16 * kBlock) return S2C(16);
+    if (f <= 28 * kBlock) return S2C(28);
     if (f <= 32 * kBlock) return S2C(32);
     return S2C(64);
 #undef S2C

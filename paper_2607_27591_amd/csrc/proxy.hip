@@ -15,11 +15,12 @@
 // both rows' contiguous segments, i.e. the same 8 proxy columns of two input
 // rows.  For INT4 the two rows' bytes are interleaved with v_perm and each
 // nibble pair is OR-ed under the exponent of 128.0 (bf16) or 1024.0 (fp16):
-// that is the exact 16-bit pair
-// (M + n_a, M + n_b), n = q + 8, and one dot2 accumulates
-// x_a (M + n_a) + x_b (M + n_b) in fp32.  (M + 8) * sum(x) is subtracted and
-// the group's scale applied once per group, column and lane group.  Lane groups and waves
-// are summed in a fixed order, so results are deterministic.
+// that is the exact 16-bit pair (M + n_a, M + n_b), n = q + 8, and one dot2
+// accumulates x_a (M + n_a) + x_b (M + n_b) in fp32.  (M + 8) * sum(x) is
+// subtracted and the group's scale applied once per group, column and lane
+// group.  Lane groups and waves are summed in a fixed order, so results are
+// deterministic.  This kernel takes up to 4 batch rows per launch; five or
+// more rows with an INT4 proxy go to proxy_mfma_kernel (the matrix cores).
 #include "common.hpp"
 #include "kernels.hpp"
 #include "topk.hpp"

@@ -5,14 +5,18 @@
 //  prologue  (sparse only) every workgroup finds the channel threshold of the
 //            top-k_ff proxy scores itself, and the ascending global position
 //            of every kept channel, so it can take exactly its slice of the
-//            kept list (balanced to +-1 channel) without another launch.
+//            kept list (balanced to +-1 channel) without another launch.  When
+//            a batch takes several launches, the first writes the kept list
+//            to the workspace and the later ones read their slice from it.
 //  gate/up   the slice's channels are cut into (channel, part of d) units
 //            spread over the 16 waves; each unit streams two contiguous rows
 //            with 16-byte loads and dot2 instructions (fp32 accumulation);
-//            s_j = SiLU(g_j) u_j is kept in LDS in fp32.
+//            s_j = act(g_j) u_j is kept in LDS in fp32.
 //  down      every thread owns 8 output columns and accumulates
 //            s_j W_down[j, c..c+8] over the slice; the workgroup writes one
 //            partial y.
+// With INT4 base weights (WQ = 4) the two streaming loops read codes and
+// per-group scales instead of 16-bit rows and dequantise on the fly.
 // reduce_kernel sums the partial y of all workgroups in workgroup order and
 // rounds y once.  No floating-point atomics: results are deterministic.
 #include "common.hpp"

@@ -109,6 +109,44 @@ def test_w4_dense_parity_and_full_keep(case):
     assert np.array_equal(y_full, y_dense)
 
 
+def _check_w4(c, w4, x_bits, k_in, k_ff, out, tag):
+    cfg = c.cfg
+    y, mask, in_mask, scores = out
+    ref = oracle.ffn_sparse_w4(x_bits, cfg.dtype, w4, k_in, k_ff, codes_g=c.codes_g,
+                               scales_g=c.scales_g, codes_u=c.codes_u, scales_u=c.scales_u,
+                               group=cfg.group, act=c.act)
+    assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"]), f"{tag}: input top-k"
+    gpu_sel = oracle.topk(scores.astype(np.float64), k_ff)
+    assert np.array_equal(np.flatnonzero(mask), gpu_sel), f"{tag}: select on GPU scores"
+    serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
+    assert serr <= SCORE_TOL * max(ref["score"].max(), 1e-30), f"{tag}: score err {serr}"
+    _, y_ref = oracle.stage2_w4(x_bits, cfg.dtype, w4, gpu_sel.astype(np.int32), c.act)
+    err = y_rel_err(y, y_ref, cfg.dtype)
+    assert err <= Y_TOL, f"{tag}: y err {err}"
+
+
+def test_w4_extreme_k(case):
+    c, q, w4 = case
+    cfg = c.cfg
+    x = c.wl.x_vectors(1, cfg.batch)[0]
+    for k_in, k_ff in [(1, 1), (1, cfg.d_ff), (cfg.d_model, 1), (cfg.d_model // 2 + 1, cfg.d_ff - 1)]:
+        log(f"[w4 extreme] {cfg.name} k_in={k_in} k_ff={k_ff}")
+        _check_w4(c, w4, x, k_in, k_ff, _run_w4(c, q, x, k_in, k_ff), f"k_in={k_in} k_ff={k_ff}")
+
+
+def test_w4_zero_input(case):
+    # All magnitudes tie at zero: the lowest indices are kept, and y is 0.
+    c, q, w4 = case
+    cfg = c.cfg
+    x = np.zeros((cfg.batch, cfg.d_model), np.uint16)
+    k_in, k_ff = min(100, cfg.d_model), min(200, cfg.d_ff)
+    y, mask, in_mask, scores = _run_w4(c, q, x, k_in, k_ff)
+    assert np.flatnonzero(in_mask).tolist() == list(range(k_in))
+    assert np.flatnonzero(mask).tolist() == list(range(k_ff))
+    assert not scores.any()
+    assert not W.bits_to_f32(y, cfg.dtype).any()
+
+
 def test_w4_threshold_mode(case):
     # Thresholds in place of counts (prox_ffn_sparse_tau_w4): the masks follow
     # the rule exactly on the GPU's own values, y is the oracle's W4 Stage 2 on

@@ -174,10 +174,15 @@ prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int 
     for (int c0 = 0; c0 < batch; c0 += pnb) {
         const int nb = batch - c0 < pnb ? batch - c0 : pnb;
         const Select in_sel{rules.tau_mode, rules.tau_x, rules.counts};
+        // With several matrix-core launches only the first selects; its list
+        // of kept rows goes to the partial-y area, which Stage 2 writes only
+        // after the last Stage 1 launch.
+        const int list_mode = batch <= pnb ? kListNone : c0 == 0 ? kListWrite : kListRead;
         if (mfma_rows)
             PROX_TRY(launch_proxy_mfma(dt, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
                                        c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel,
-                                       m.act, stream));
+                                       m.act, reinterpret_cast<int32_t *>(W.ypart), list_mode,
+                                       stream));
         else
             PROX_TRY(launch_proxy(dt, qbits, x, batch, c0, nb, d, f, p->group, k_in, p->blob,
                                   c0 == 0 ? in_mask : nullptr, W.scores, c0 > 0, in_sel, m.act,

@@ -28,10 +28,14 @@ hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int 
 // with nb <= proxy_mfma_rows(d, group, k_in) (16, 8, or 0 when the kept-row
 // list does not fit in LDS); otherwise as launch_proxy.
 int proxy_mfma_rows(int d, int group, int k_in);
+// klist, list_mode: as Stage 2's kept list (KeptList), for the input rows:
+// the first launch of a call with several also writes the kept rows in
+// ascending order to klist[0..n) and n to klist[d]; the later ones rebuild
+// their list from it instead of selecting again.
 hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, int nb, int d,
                              int f, int group, int k_in, const void *blob, uint8_t *in_mask,
-                             float *scores, int accumulate, Select sel, int act,
-                             hipStream_t stream);
+                             float *scores, int accumulate, Select sel, int act, int32_t *klist,
+                             int list_mode, hipStream_t stream);
 constexpr int kProxyMfmaMinRows = 5;   // batch rows from which Stage 1 uses the matrix cores
 
 // The three matrices of Stage 2: channel-major 16-bit rows (wq == 16), or

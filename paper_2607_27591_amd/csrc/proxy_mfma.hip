@@ -69,7 +69,8 @@ template <int DT, int T, int C, int NX>
 __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     const uint16_t *__restrict__ x_all, int B_all, int row0, int nb, int d, int f, int group,
     int k_in, const uint8_t *__restrict__ blob, uint8_t *__restrict__ in_mask,
-    float *__restrict__ scores, int accumulate, Select sel_rule, int act) {
+    float *__restrict__ scores, int accumulate, Select sel_rule, int act,
+    int32_t *__restrict__ klist, int list_mode) {   // kept-row list of a multi-launch call
     static_assert(T == 64 || T == 128, "tile widths of the blob layout");
     static_assert(NX == 8 || NX == 16, "x rows kept in LDS");
     constexpr int WH = T / 64;                       // 64-column halves per tile
@@ -93,87 +94,122 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     uint16_t *kbg_sh = reinterpret_cast<uint16_t *>(dsm + align_up((size_t)cap * 2, 16) +
                                                     align_up((size_t)NX * cap * 2, 16));
 
-    // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
-    // x is read XQ rows at a time so their loads are in flight together.
-    constexpr int XQ = C <= 8 ? 4 : 2;
-    uint32_t key[C];
-#pragma unroll
-    for (int r = 0; r < C; ++r) key[r] = 0u;
-    for (int b0 = 0; b0 < B_all; b0 += XQ) {
-        uint32_t raw[XQ][C];
-#pragma unroll
-        for (int q = 0; q < XQ; ++q) {
-            const uint16_t *xb = x_all + (size_t)min(b0 + q, B_all - 1) * d;
-#pragma unroll
-            for (int r = 0; r < C; ++r) raw[q][r] = xb[min(r * kBlock + tid, d - 1)];
+    // List start of each group: the kept counts padded to whole blocks, scanned.
+    auto group_starts = [&]() {
+        if (wid == 0) {
+            int carry = 0;
+            for (int g0 = 0; g0 <= ng; g0 += kWave) {
+                const int g = g0 + lane;
+                const int cnt = g < ng ? gsel0[g + 1] - gsel0[g] : 0;
+                const int padded = (cnt + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
+                const int incl = wave_inclusive_scan(padded);
+                if (g <= ng) gstart[g] = carry + incl - padded;
+                carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+            }
         }
-#pragma unroll
-        for (int q = 0; q < XQ; ++q)
+        __syncthreads();
+    };
+    const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;   // i / group, exact here
+    if (list_mode == kListRead) {
+        // Another launch of this call selected: its list (ascending kept rows,
+        // count at klist[d]) gives the same groups and list positions.
+        const int n = klist[d];
+        for (int g = tid; g <= ng; g += kBlock) {   // kept rows below g * group
+            const int v = g * group;
+            int lo = 0, hi = n;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (klist[mid] < v) lo = mid + 1;
+                else hi = mid;
+            }
+            gsel0[g] = lo;
+        }
+        __syncthreads();
+        group_starts();
+        for (int idx = tid; idx < n; idx += kBlock) {
+            const int i = klist[idx];
+            const int g = (int)__umulhi((uint32_t)i, gmagic);
+            const int p = gstart[g] + idx - gsel0[g];
+            rows_sh[p] = (uint16_t)i;
+            for (int b = 0; b < nb; ++b) xs_sh[b * cap + p] = x_all[(size_t)(row0 + b) * d + i];
+        }
+    } else {
+        // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
+        // x is read XQ rows at a time so their loads are in flight together.
+        constexpr int XQ = C <= 8 ? 4 : 2;
+        uint32_t key[C];
+    #pragma unroll
+        for (int r = 0; r < C; ++r) key[r] = 0u;
+        for (int b0 = 0; b0 < B_all; b0 += XQ) {
+            uint32_t raw[XQ][C];
+    #pragma unroll
+            for (int q = 0; q < XQ; ++q) {
+                const uint16_t *xb = x_all + (size_t)min(b0 + q, B_all - 1) * d;
+    #pragma unroll
+                for (int r = 0; r < C; ++r) raw[q][r] = xb[min(r * kBlock + tid, d - 1)];
+            }
+    #pragma unroll
+            for (int q = 0; q < XQ; ++q)
+    #pragma unroll
+                for (int r = 0; r < C; ++r)
+                    if (r * kBlock + tid < d) key[r] = max(key[r], raw[q][r] & 0x7FFFu);
+        }
+        uint64_t sel = 0;
+        if (sel_rule.tau_mode) {
+    #pragma unroll
+            for (int r = 0; r < C; ++r) {
+                const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
+                sel |= (uint64_t)in << r;
+            }
+            topk_order<kBlock, C>(sel, d, tk, ord);
+            if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
+                *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
+        } else {
+            sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+        }
+
+        // ---- groups: kept rows per group, list starts padded to whole blocks ----
+        for (int g = tid; g <= ng; g += kBlock) gsel0[g] = topk_selected_before<kBlock, C>(ord, g * group);
+        __syncthreads();
+        group_starts();
+
+        // ---- kept rows and their x values to the list ----
+        auto list_pos = [&](int r) {
+            const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
+            return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
+        };
+        int pos[C];   // list position of each of this thread's inputs, -1 if not kept
+    #pragma unroll
+        for (int r = 0; r < C; ++r) {
+            const int i = r * kBlock + tid;
+            const bool s = i < d && ((sel >> r) & 1);
+            pos[r] = s ? list_pos(r) : -1;
+            if (tile == 0 && in_mask && i < d) in_mask[i] = s ? 1 : 0;
+            if (s) rows_sh[pos[r]] = (uint16_t)i;
+        }
+        // Only the nb real batch rows are stored: the stream feeds zeros for the
+        // others.
+        for (int b0 = 0; b0 < nb; b0 += XQ) {
+            uint16_t xv[XQ][C];
+    #pragma unroll
+            for (int q = 0; q < XQ; ++q) {
+                const uint16_t *xb = x_all + (size_t)(row0 + min(b0 + q, nb - 1)) * d;
+    #pragma unroll
+                for (int r = 0; r < C; ++r) xv[q][r] = xb[min(r * kBlock + tid, d - 1)];
+            }
+    #pragma unroll
+            for (int q = 0; q < XQ; ++q)
+                if (b0 + q < nb)
+    #pragma unroll
+                    for (int r = 0; r < C; ++r)
+                        if (pos[r] >= 0) xs_sh[(b0 + q) * cap + pos[r]] = xv[q][r];
+        }
+        if (list_mode == kListWrite && tile == 0) {   // the list for the later launches
 #pragma unroll
             for (int r = 0; r < C; ++r)
-                if (r * kBlock + tid < d) key[r] = max(key[r], raw[q][r] & 0x7FFFu);
-    }
-    uint64_t sel = 0;
-    if (sel_rule.tau_mode) {
-#pragma unroll
-        for (int r = 0; r < C; ++r) {
-            const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
-            sel |= (uint64_t)in << r;
+                if (pos[r] >= 0) klist[topk_pos<C>(ord, r)] = r * kBlock + tid;
+            if (tid == 0) klist[d] = gsel0[ng];
         }
-        topk_order<kBlock, C>(sel, d, tk, ord);
-        if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
-            *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
-    } else {
-        sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
-    }
-
-    // ---- groups: kept rows per group, list starts padded to whole blocks ----
-    for (int g = tid; g <= ng; g += kBlock) gsel0[g] = topk_selected_before<kBlock, C>(ord, g * group);
-    __syncthreads();
-    if (wid == 0) {
-        int carry = 0;
-        for (int g0 = 0; g0 <= ng; g0 += kWave) {
-            const int g = g0 + lane;
-            const int cnt = g < ng ? gsel0[g + 1] - gsel0[g] : 0;
-            const int padded = (cnt + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
-            const int incl = wave_inclusive_scan(padded);
-            if (g <= ng) gstart[g] = carry + incl - padded;
-            carry += __builtin_amdgcn_readlane(incl, kWave - 1);
-        }
-    }
-    __syncthreads();
-
-    // ---- kept rows and their x values to the list ----
-    const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;   // i / group, exact here
-    auto list_pos = [&](int r) {
-        const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
-        return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
-    };
-    int pos[C];   // list position of each of this thread's inputs, -1 if not kept
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-        const int i = r * kBlock + tid;
-        const bool s = i < d && ((sel >> r) & 1);
-        pos[r] = s ? list_pos(r) : -1;
-        if (tile == 0 && in_mask && i < d) in_mask[i] = s ? 1 : 0;
-        if (s) rows_sh[pos[r]] = (uint16_t)i;
-    }
-    // Only the nb real batch rows are stored: the stream feeds zeros for the
-    // others.
-    for (int b0 = 0; b0 < nb; b0 += XQ) {
-        uint16_t xv[XQ][C];
-#pragma unroll
-        for (int q = 0; q < XQ; ++q) {
-            const uint16_t *xb = x_all + (size_t)(row0 + min(b0 + q, nb - 1)) * d;
-#pragma unroll
-            for (int r = 0; r < C; ++r) xv[q][r] = xb[min(r * kBlock + tid, d - 1)];
-        }
-#pragma unroll
-        for (int q = 0; q < XQ; ++q)
-            if (b0 + q < nb)
-#pragma unroll
-                for (int r = 0; r < C; ++r)
-                    if (pos[r] >= 0) xs_sh[(b0 + q) * cap + pos[r]] = xv[q][r];
     }
     __syncthreads();   // the kept rows are in place: pads copy the group's last one
     for (int g = tid; g < ng; g += kBlock) {
@@ -318,7 +354,8 @@ int proxy_mfma_rows(int d, int group, int k_in) {
 template <int DT, int T, int C, int NX>
 static hipError_t launch_mfma_t(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                 int group, int k_in, const void *blob, uint8_t *in_mask,
-                                float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+                                float *scores, int accumulate, Select sel, int act,
+                                int32_t *klist, int list_mode, hipStream_t s) {
     const BlobLayout L(d, f, 4, group);
     const size_t lds = mfma_lds_bytes(k_in, d / group, NX);
     const hipError_t e = hipFuncSetAttribute(
@@ -327,16 +364,17 @@ static hipError_t launch_mfma_t(const void *x_all, int B_all, int row0, int nb, 
     if (e != hipSuccess) return e;
     proxy_mfma_kernel<DT, T, C, NX><<<L.n_tiles, kBlock, lds, s>>>(
         static_cast<const uint16_t *>(x_all), B_all, row0, nb, d, f, group, k_in,
-        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel, act);
+        static_cast<const uint8_t *>(blob), in_mask, scores, accumulate, sel, act, klist, list_mode);
     return hipGetLastError();
 }
 
 template <int DT, int T>
 static hipError_t launch_mfma_c(const void *x_all, int B_all, int row0, int nb, int d, int f,
                                 int group, int k_in, const void *blob, uint8_t *in_mask,
-                                float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+                                float *scores, int accumulate, Select sel, int act,
+                                int32_t *klist, int list_mode, hipStream_t s) {
     const int nx = proxy_mfma_rows(d, group, k_in);
-#define MF(C_, NX_) launch_mfma_t<DT, T, C_, NX_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
+#define MF(C_, NX_) launch_mfma_t<DT, T, C_, NX_>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, klist, list_mode, s)
     if (d <= 4 * kBlock) return nx == 16 ? MF(4, 16) : MF(4, 8);
     if (d <= 8 * kBlock) return nx == 16 ? MF(8, 16) : MF(8, 8);
     return nx == 16 ? MF(16, 16) : MF(16, 8);
@@ -345,13 +383,15 @@ static hipError_t launch_mfma_c(const void *x_all, int B_all, int row0, int nb, 
 
 hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, int nb, int d,
                              int f, int group, int k_in, const void *blob, uint8_t *in_mask,
-                             float *scores, int accumulate, Select sel, int act, hipStream_t s) {
+                             float *scores, int accumulate, Select sel, int act, int32_t *klist,
+                             int list_mode, hipStream_t s) {
     if (nb < 1 || nb > proxy_mfma_rows(d, group, k_in)) return hipErrorInvalidValue;
+    if (list_mode != kListNone && !klist) return hipErrorInvalidValue;
     if (proxy_tile(f) == 128)
-        return dtype == kBF16 ? launch_mfma_c<kBF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
-                              : launch_mfma_c<kF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s);
-    return dtype == kBF16 ? launch_mfma_c<kBF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s)
-                          : launch_mfma_c<kF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, s);
+        return dtype == kBF16 ? launch_mfma_c<kBF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, klist, list_mode, s)
+                              : launch_mfma_c<kF16, 128>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, klist, list_mode, s);
+    return dtype == kBF16 ? launch_mfma_c<kBF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, klist, list_mode, s)
+                          : launch_mfma_c<kF16, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel, act, klist, list_mode, s);
 }
 
 }  // namespace prox

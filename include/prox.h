@@ -140,6 +140,18 @@ size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
 int prox_stage1_mfma_rows(int d_model, prox_qfmt fmt, int group, int batch, int k_in);
 
 /*
+ * Which Stage-2 kernel a call takes (for inspection and tests): the batch rows
+ * one Stage-2 launch covers.  16 means the matrix-core kernel (more than eight
+ * batch rows of 16-bit weights with d_model >= 4096: gate/up as 16x16x16
+ * MFMAs, the three matrices read once per 16 rows); otherwise the VALU kernel
+ * takes up to 8 rows per launch (fewer for INT4 weights, w4 != 0, at wide
+ * d_model), and a batch tail of 8 rows or fewer always runs on it.  0 for an
+ * unsupported shape or batch.  Host only, no HIP calls.  Both kernels give
+ * the same kept set; y differs only in fp32 summation order.
+ */
+int prox_stage2_rows(int d_model, int d_ff, int w4, int batch);
+
+/*
  * Dense SwiGLU FFN (Sec. 2.1):  y = (x W_up (.) SiLU(x W_gate)) W_down.
  *   x: device [batch][d_model], w->dtype;  y: device [batch][d_model], same
  *   dtype, rounded once (round-to-nearest-even) from fp32 accumulation.

@@ -98,6 +98,11 @@ Ws carve(void *ws, int d, int f, int batch) {
 const char *const kStageNames[PROX_SPARSE_STAGES] = {"proxy_gemv_score",
                                                      "stage2_select_gate_up_down", "reduce_y"};
 
+// Batch rows per Stage 2 launch for a call of `batch` rows.
+int stage2_launch_rows(int d, int wq, int batch) {
+    return batch > kStage2MaxNB && stage2_mfma_ok(d, wq) ? kStage2MfmaRows : stage2_rows(d, wq);
+}
+
 // Stage 2 and the final reduction, shared by the sparse and the dense FFN
 // (scores == NULL: every channel).
 prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff,
@@ -109,16 +114,24 @@ prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff
     // grid for every channel (workgroups past the count get no channels).
     const int nwg = stage2_wgs(scores && !sel.tau_mode ? k_ff : f);
     const int ystride = ypart_rows(batch);
-    const int rows = stage2_rows(d, m.s2.wq);
+    // More than eight rows of 16-bit weights: the matrix-core kernel, up to
+    // 16 rows per launch (a tail of eight or fewer rows takes the VALU kernel).
+    const int rows = stage2_launch_rows(d, m.s2.wq, batch);
     for (int c0 = 0; c0 < batch; c0 += rows) {
         const int nb = batch - c0 < rows ? batch - c0 : rows;
         const int list_mode = !scores || rows >= batch ? kListNone
                               : c0 == 0             ? kListWrite
                                                     : kListRead;
-        PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
-                               c0 == 0 ? scores_copy : nullptr, W.ypart + (size_t)c0 * d, ystride,
-                               nwg, c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, m.act,
-                               W.klist, list_mode, stream));
+        const Select sl = c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr};
+        float *const sc = c0 == 0 ? scores_copy : nullptr;
+        if (nb > kStage2MaxNB)
+            PROX_TRY(launch_stage2_mfma(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff,
+                                        mask, sc, W.ypart + (size_t)c0 * d, ystride, nwg, sl,
+                                        m.act, W.klist, list_mode, stream));
+        else
+            PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
+                                   sc, W.ypart + (size_t)c0 * d, ystride, nwg, sl, m.act,
+                                   W.klist, list_mode, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
     PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));
@@ -229,6 +242,11 @@ int prox_stage1_mfma_rows(int d_model, prox_qfmt fmt, int group, int batch, int 
         batch < 1 || batch > PROX_MAX_BATCH || k_in < 1 || k_in > d_model)
         return 0;
     return stage1_mfma_rows(d_model, qbits_of(fmt), group, batch, k_in);
+}
+
+int prox_stage2_rows(int d_model, int d_ff, int w4, int batch) {
+    if (!shape_ok(d_model, d_ff) || batch < 1 || batch > PROX_MAX_BATCH) return 0;
+    return stage2_launch_rows(d_model, w4 ? 4 : 16, batch);
 }
 
 size_t prox_proxy_bytes(int d_model, int d_ff, prox_qfmt fmt, int group) {

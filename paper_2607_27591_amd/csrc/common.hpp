@@ -87,6 +87,23 @@ struct Int4Magic<kF16> {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// D += A B on the matrix cores, 16 x 16 x 16 with fp32 accumulation.  Lane l
+// holds A[l % 16][4 (l / 16) + e] and B[4 (l / 16) + e][l % 16] for e = 0..3
+// (four 16-bit values in a uint2) and gets D[4 (l / 16) + e][l % 16].
+template <int DT>
+__device__ __forceinline__ v4f mfma16(uint2 a, uint2 b, v4f c) {
+    if constexpr (DT == kBF16)
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(v4s, a),
+                                                         __builtin_bit_cast(v4s, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a),
+                                                     __builtin_bit_cast(v4h, b), c, 0, 0, 0);
+}
+
 // 16-byte streaming load (non-temporal hint: weights are read once per call).
 __device__ __forceinline__ uint4 load_stream16(const void *p) {
     const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));

@@ -63,6 +63,15 @@ hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const S
                          const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                          float *ypart, int ystride, int nwg, Select sel, int act,
                          int32_t *klist, int klist_mode, hipStream_t stream);
+// The same Stage 2 for 9 to kStage2MfmaRows batch rows in one launch, with
+// gate/up on the matrix cores; 16-bit weights and d >= 4096 only
+// (stage2_mfma_ok).  Same arguments, workspace layout and kept-list modes.
+bool stage2_mfma_ok(int d, int wq);
+hipError_t launch_stage2_mfma(int dtype, const void *x, int nb, int d, int f,
+                              const Stage2Weights &w, const float *scores, int k_ff,
+                              uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                              int nwg, Select sel, int act, int32_t *klist, int klist_mode,
+                              hipStream_t stream);
 // INT4 base weights: quantise W_gate, W_up, W_down (channel-major [f][d]) into
 // a W4Layout blob, and the inverse view of matrix m (0 gate, 1 up, 2 down).
 hipError_t launch_pack_w4(int dtype, const void *wg, const void *wu, const void *wd, int d, int f,

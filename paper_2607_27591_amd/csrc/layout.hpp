@@ -106,6 +106,7 @@ struct W4Layout {
 };
 
 constexpr int kStage2MaxNB = 8;          // batch rows per Stage 2 launch
+constexpr int kStage2MfmaRows = 16;      // ... of the matrix-core Stage 2 (16-bit weights)
 
 // Batch rows a Stage 2 launch of nb <= 8 rows is compiled for (1, 2, 4 or 8).
 __host__ __device__ inline int stage2_nb_t(int nb) {

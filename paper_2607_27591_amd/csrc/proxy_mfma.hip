@@ -30,24 +30,11 @@
 
 namespace prox {
 
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef _Float16 v4h __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned short us2 __attribute__((ext_vector_type(2)));   // two rows' codes, one VGPR
 
 constexpr int kMfmaBlock = 16;    // kept input rows per block (the MFMA's K)
 constexpr int kMfmaU = 4;         // blocks in flight per wave
 
-
-template <int DT>
-__device__ __forceinline__ v4f mfma16(uint2 a, uint2 b, v4f c) {
-    if constexpr (DT == kBF16)
-        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(v4s, a),
-                                                         __builtin_bit_cast(v4s, b), c, 0, 0, 0);
-    else
-        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a),
-                                                     __builtin_bit_cast(v4h, b), c, 0, 0, 0);
-}
 
 // Dynamic LDS: rows [cap] u16, x [NX][cap] u16, block groups [cap / 16] u16;
 // after the stream the same space holds the cross-wave partial sums

@@ -62,20 +62,18 @@ struct Stage2Smem {
     float gu[kMaxSlice * kMaxParts * 2 * 2];   // [t][q][b][2] for nbt <= 2
 };
 
-// WQ: 16 for 16-bit weights, 4 for INT4 codes (wt.sg/su/sd: their scales).
-template <int NB, int DT, int C, int WQ>
-__global__ __launch_bounds__(kBlock) void stage2_kernel(
-    const uint16_t *__restrict__ x, int nb, int d, int f, Stage2Weights wt,
-    const float *__restrict__ scores,   // NULL: dense FFN over all f channels
-    int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
-    float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
-    Select sel_rule, int act,                       // act: gate activation
-    int32_t *__restrict__ klist, int klist_mode) {  // kept-channel list, KeptList mode
-    static_assert(WQ == 16 || WQ == 4, "16-bit or INT4 weights");
-    const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
-    const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
-    const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
-    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+// The selection prologue of both Stage 2 kernels: this workgroup's slice of the
+// kept channels (their ids to list[0..n), n returned) and its chunk of the mask.
+// Every workgroup ranks the scores itself (top-k or the threshold rule), or,
+// for the later launches of a multi-launch batch, reads the first launch's list.
+// The caller synchronises before reading list.
+template <int C>
+__device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, int f, int k_ff,
+                                            uint8_t *__restrict__ mask,
+                                            float *__restrict__ scores_copy, Select sel_rule,
+                                            int32_t *__restrict__ klist, int klist_mode,
+                                            TopKScratch &tk, TopKOrder<C> &ord, int *list) {
+    const int tid = threadIdx.x;
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
     // Channels of this workgroup: an even share of the n_ch kept channels
@@ -84,10 +82,6 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     int p0 = (int)((long long)w * n_ch / nwg), p1 = (int)((long long)(w + 1) * n_ch / nwg);
     int n = p1 - p0;
 
-    __shared__ TopKScratch tk;
-    __shared__ TopKOrder<C> ord;
-    __shared__ Stage2Smem sm;
-    extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
 
     // ---- prologue: this workgroup's slice of the kept channels ----
     if (sparse && klist_mode == kListRead) {
@@ -100,7 +94,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
             p1 = w < nwg_k ? (int)((long long)(w + 1) * n_ch / nwg_k) : n_ch;
             n = p1 - p0;
         }
-        for (int t = tid; t < n; t += kBlock) sm.list[t] = klist[p0 + t];
+        for (int t = tid; t < n; t += kBlock) list[t] = klist[p0 + t];
         __syncthreads();
     } else if (sparse) {
         // Item r of thread t is channel r * kBlock + t (coalesced loads).
@@ -134,8 +128,8 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         // This workgroup's slice of positions and its chunk of the mask,
         // straight from the order tables.
         for (int t = tid; t < n; t += kBlock) {
-            sm.list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
-            if (klist_mode == kListWrite) klist[p0 + t] = sm.list[t];
+            list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
+            if (klist_mode == kListWrite) klist[p0 + t] = list[t];
         }
         if (klist_mode == kListWrite && w == 0 && tid == 0) klist[f] = n_ch;
         const int mchunk = (f + nwg - 1) / nwg;   // mask entries written by this workgroup
@@ -147,8 +141,34 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         (void)sel;
         __syncthreads();
     } else {
-        for (int t = tid; t < n; t += kBlock) sm.list[t] = p0 + t;
+        for (int t = tid; t < n; t += kBlock) list[t] = p0 + t;
     }
+
+    return n;
+}
+
+// WQ: 16 for 16-bit weights, 4 for INT4 codes (wt.sg/su/sd: their scales).
+template <int NB, int DT, int C, int WQ>
+__global__ __launch_bounds__(kBlock) void stage2_kernel(
+    const uint16_t *__restrict__ x, int nb, int d, int f, Stage2Weights wt,
+    const float *__restrict__ scores,   // NULL: dense FFN over all f channels
+    int k_ff, uint8_t *__restrict__ mask, float *__restrict__ scores_copy,
+    float *__restrict__ ypart, int ypart_stride,   // partial y rows per workgroup
+    Select sel_rule, int act,                       // act: gate activation
+    int32_t *__restrict__ klist, int klist_mode) {  // kept-channel list, KeptList mode
+    static_assert(WQ == 16 || WQ == 4, "16-bit or INT4 weights");
+    const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
+    const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
+    const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+
+    __shared__ TopKScratch tk;
+    __shared__ TopKOrder<C> ord;
+    __shared__ Stage2Smem sm;
+    extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
+
+    const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
+                                  klist_mode, tk, ord, sm.list);
 
     const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
     uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
@@ -458,10 +478,175 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 if (b < nb) {
-                    float4 *dst = reinterpret_cast<float4 *>(ypart + ((size_t)w * ypart_stride + b) * d + cg * 8);
+                    float4 *dst = reinterpret_cast<float4 *>(ypart + ((size_t)blockIdx.x * ypart_stride + b) * d + cg * 8);
                     dst[0] = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
                     dst[1] = make_float4(acc[b][4], acc[b][5], acc[b][6], acc[b][7]);
                 }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// stage2_mfma_kernel: Stage 2 for 9 to 16 batch rows of 16-bit weights in one
+// launch, so every kept row of the three matrices is read once for all rows.
+//  prologue  the slice of kept channels, as in stage2_kernel.
+//  gate/up   on the matrix cores: the slice is cut into tiles of 16 channels,
+//            and wave w takes the w-th sixteenth of d for every tile, so the
+//            waves stream equal bytes however few channels the slice holds.
+//            Per 32 inputs a lane loads 16 contiguous bytes of one channel row
+//            of each matrix (A) and of one batch row of x (B, from L2), and two
+//            16 x 16 x 16 MFMAs per matrix add the products into the tile's
+//            [16 channels][16 rows] fp32 sums.  The 16 waves' sums of a tile
+//            are added through LDS in wave order; s = act(g) u goes to LDS.
+//  down      VALU: every thread owns 4 output columns and all 16 rows.
+// ---------------------------------------------------------------------------
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+constexpr int kS2mTiles = 2;   // channel tiles per pass through the gate/up loop
+constexpr int kS2mRed = kS2mTiles * 2 * kMaxBlockWaves * kWave;   // float4 per pass
+
+size_t stage2_mfma_lds_bytes() {
+    return (size_t)kS2mRed * 16 + (size_t)kMaxSlice * kStage2MfmaRows * 4;
+}
+
+bool stage2_mfma_ok(int d, int wq) { return wq == 16 && d >= 4 * kBlock; }
+
+template <int DT, int C>
+__global__ __launch_bounds__(kBlock) void stage2_mfma_kernel(
+    const uint16_t *__restrict__ x, int nb, int d, int f, Stage2Weights wt,
+    const float *__restrict__ scores, int k_ff, uint8_t *__restrict__ mask,
+    float *__restrict__ scores_copy, float *__restrict__ ypart, int ypart_stride,
+    Select sel_rule, int act, int32_t *__restrict__ klist, int klist_mode) {
+    constexpr int R = kStage2MfmaRows;
+    const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
+    const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
+    const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
+    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
+
+    __shared__ TopKScratch tk;
+    __shared__ TopKOrder<C> ord;
+    __shared__ int list[kMaxSlice];
+    extern __shared__ __align__(16) float dyn[];   // red [tiles][2][waves][lanes] float4 | s [slice][R]
+    float4 *red = reinterpret_cast<float4 *>(dyn);
+    float *s_sh = dyn + (size_t)kS2mRed * 4;
+
+    const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
+                                  klist_mode, tk, ord, list);
+    __syncthreads();
+
+    // ---- gate/up ----
+    const int nsteps = d / 32;   // steps of 32 inputs
+    const int k_lo = wid * nsteps / kMaxBlockWaves, k_hi = (wid + 1) * nsteps / kMaxBlockWaves;
+    const int r = lane % 16, g4 = lane / 16;
+    const bool xrow = r < nb;
+    const uint16_t *xr = x + (size_t)(xrow ? r : 0) * d + 8 * g4;
+    const int ntiles = (n + 15) / 16;
+    constexpr int U = 2;   // steps in flight per lane
+    for (int t0 = 0; t0 < ntiles; t0 += kS2mTiles) {
+        const uint16_t *rg[kS2mTiles], *ru[kS2mTiles];
+        bool live[kS2mTiles];
+        v4f ag[kS2mTiles], au[kS2mTiles];
+#pragma unroll
+        for (int tt = 0; tt < kS2mTiles; ++tt) {
+            const int t = (t0 + tt) * 16 + r;
+            live[tt] = t < n;
+            const int j = live[tt] ? list[t] : 0;
+            rg[tt] = wg + (size_t)j * d + 8 * g4;
+            ru[tt] = wu + (size_t)j * d + 8 * g4;
+            ag[tt] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+            au[tt] = ag[tt];
+        }
+        for (int k = k_lo; k < k_hi; k += U) {
+            uint4 xv[U], gv[kS2mTiles][U], uv[kS2mTiles][U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int kk = k + u;
+                const bool in = kk < k_hi;
+                xv[u] = in && xrow ? *reinterpret_cast<const uint4 *>(xr + kk * 32) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+                for (int tt = 0; tt < kS2mTiles; ++tt) {
+                    const bool ld = in && live[tt];
+                    gv[tt][u] = ld ? load_stream16(rg[tt] + kk * 32) : make_uint4(0, 0, 0, 0);
+                    uv[tt][u] = ld ? load_stream16(ru[tt] + kk * 32) : make_uint4(0, 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                // Inputs 8 g4 + 0..3 of the step in the first MFMA, 8 g4 + 4..7
+                // in the second: A and B take the same inputs in the same slots.
+                const uint2 xa = make_uint2(xv[u].x, xv[u].y), xb = make_uint2(xv[u].z, xv[u].w);
+#pragma unroll
+                for (int tt = 0; tt < kS2mTiles; ++tt) {
+                    ag[tt] = mfma16<DT>(make_uint2(gv[tt][u].x, gv[tt][u].y), xa, ag[tt]);
+                    ag[tt] = mfma16<DT>(make_uint2(gv[tt][u].z, gv[tt][u].w), xb, ag[tt]);
+                    au[tt] = mfma16<DT>(make_uint2(uv[tt][u].x, uv[tt][u].y), xa, au[tt]);
+                    au[tt] = mfma16<DT>(make_uint2(uv[tt][u].z, uv[tt][u].w), xb, au[tt]);
+                }
+            }
+        }
+        // Lane l holds channel 4 (l / 16) + e, batch row l % 16 of each tile.
+#pragma unroll
+        for (int tt = 0; tt < kS2mTiles; ++tt) {
+            red[((tt * 2 + 0) * kMaxBlockWaves + wid) * kWave + lane] =
+                make_float4(ag[tt][0], ag[tt][1], ag[tt][2], ag[tt][3]);
+            red[((tt * 2 + 1) * kMaxBlockWaves + wid) * kWave + lane] =
+                make_float4(au[tt][0], au[tt][1], au[tt][2], au[tt][3]);
+        }
+        __syncthreads();
+        if (tid < kS2mTiles * kWave * 4) {
+            const int tt = tid / (kWave * 4), ln = (tid / 4) % kWave, e = tid % 4;
+            const float *rf = reinterpret_cast<const float *>(red);
+            float gs = 0.0f, us = 0.0f;
+            for (int w = 0; w < kMaxBlockWaves; ++w) {
+                gs += rf[(((tt * 2 + 0) * kMaxBlockWaves + w) * kWave + ln) * 4 + e];
+                us += rf[(((tt * 2 + 1) * kMaxBlockWaves + w) * kWave + ln) * 4 + e];
+            }
+            const int t = (t0 + tt) * 16 + 4 * (ln / 16) + e;
+            if (t < n) s_sh[t * R + ln % 16] = gate_act(gs, act) * us;
+        }
+        __syncthreads();
+    }
+
+    // ---- down: partial y over this slice, 4 columns x 16 rows per thread ----
+    constexpr int UD = 8;
+    for (int cg = tid; cg < d / 4; cg += kBlock) {
+        float acc[R][4];
+#pragma unroll
+        for (int b = 0; b < R; ++b)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
+        for (int t0 = 0; t0 < n; t0 += UD) {
+            uint2 wv[UD];
+#pragma unroll
+            for (int u = 0; u < UD; ++u) {
+                const int t = t0 + u;
+                if (t < n) {
+                    const u32x2 v = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x2 *>(wd + (size_t)list[t] * d + cg * 4));
+                    wv[u] = make_uint2(v.x, v.y);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < UD; ++u) {
+                const int t = t0 + u;
+                if (t < n) {
+                    const float wf[4] = {lo_to_float<DT>(wv[u].x), hi_to_float<DT>(wv[u].x),
+                                         lo_to_float<DT>(wv[u].y), hi_to_float<DT>(wv[u].y)};
+#pragma unroll
+                    for (int b = 0; b < R; ++b) {
+                        const float sv = s_sh[t * R + b];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < R; ++b) {
+            if (b < nb) {
+                float4 *dst = reinterpret_cast<float4 *>(
+                    ypart + ((size_t)blockIdx.x * ypart_stride + b) * d + cg * 4);
+                *dst = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
             }
         }
     }
@@ -612,6 +797,55 @@ hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const S
     S2NB(kF16, 16)
 #undef S2NB
 #undef S2
+}
+
+template <int DT, int C>
+static hipError_t launch_stage2m_t(const void *x, int nb, int d, int f, const Stage2Weights &wt,
+                                   const float *scores, int k_ff, uint8_t *mask,
+                                   float *scores_copy, float *ypart, int ystride, int nwg,
+                                   Select sel_rule, int act, int32_t *klist, int klist_mode,
+                                   hipStream_t st) {
+    const size_t lds = stage2_mfma_lds_bytes();
+    hipError_t e = allow_lds(stage2_mfma_kernel<DT, C>, lds);
+    if (e != hipSuccess) return e;
+    stage2_mfma_kernel<DT, C><<<nwg, kBlock, lds, st>>>(
+        static_cast<const uint16_t *>(x), nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
+        ystride, sel_rule, act, klist, klist_mode);
+    return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t launch_stage2m_c(const void *x, int nb, int d, int f, const Stage2Weights &wt,
+                                   const float *scores, int k_ff, uint8_t *mask,
+                                   float *scores_copy, float *ypart, int ystride, int nwg,
+                                   Select sel_rule, int act, int32_t *klist, int klist_mode,
+                                   hipStream_t st) {
+#define S2M(C_) launch_stage2m_t<DT, C_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, klist, klist_mode, st)
+    if (scores && f <= 4 * kBlock) return S2M(4);
+    if (scores && f <= 8 * kBlock) return S2M(8);
+    if (scores && f <= 12 * kBlock) return S2M(12);
+    if (!scores || f <= 16 * kBlock) return S2M(16);
+    if (f <= 28 * kBlock) return S2M(28);
+    if (f <= 32 * kBlock) return S2M(32);
+    return S2M(64);
+#undef S2M
+}
+
+hipError_t launch_stage2_mfma(int dtype, const void *x, int nb, int d, int f,
+                              const Stage2Weights &wt, const float *scores, int k_ff,
+                              uint8_t *mask, float *scores_copy, float *ypart, int ystride,
+                              int nwg, Select sel_rule, int act, int32_t *klist, int klist_mode,
+                              hipStream_t st) {
+    const int n_ch = scores && !sel_rule.tau_mode ? k_ff : f;   // the kept-list length
+    if (nb < 1 || nb > kStage2MfmaRows || !stage2_mfma_ok(d, wt.wq) || nwg < 1 ||
+        nwg > kStage2MaxWGs || (long long)n_ch > (long long)kMaxSlice * nwg)
+        return hipErrorInvalidValue;
+    if (klist_mode != kListNone && (!scores || !klist)) return hipErrorInvalidValue;
+    if (dtype == kBF16)
+        return launch_stage2m_c<kBF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
+                                       ystride, nwg, sel_rule, act, klist, klist_mode, st);
+    return launch_stage2m_c<kF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
+                                  ystride, nwg, sel_rule, act, klist, klist_mode, st);
 }
 
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,

@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         L.prox_workspace_bytes.restype = S
         L.prox_stage1_mfma_rows.argtypes = [I, I, I, I, I]
         L.prox_stage1_mfma_rows.restype = I
+        L.prox_stage2_rows.argtypes = [I, I, I, I]
+        L.prox_stage2_rows.restype = I
         L.prox_ffn_dense.argtypes = [WP, P, I, P, P, S, P]
         L.prox_ffn_sparse.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P]
         L.prox_ffn_sparse_staged.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
@@ -191,6 +193,12 @@ def stage1_mfma_rows(d_model: int, fmt: int, group: int, batch: int, k_in: int) 
     """Batch rows per matrix-core Stage-1 launch, 0 when the dot-product
     kernel runs (threshold mode: pass k_in = d_model)."""
     return int(lib().prox_stage1_mfma_rows(d_model, fmt, group, batch, k_in))
+
+
+def stage2_rows(d_model: int, d_ff: int, w4: bool, batch: int) -> int:
+    """Batch rows per Stage-2 launch: 16 on the matrix-core kernel, else the
+    VALU kernel's row count; 0 for an unsupported shape or batch."""
+    return int(lib().prox_stage2_rows(d_model, d_ff, int(w4), batch))
 
 
 def workspace_bytes(d_model: int, d_ff: int, batch: int) -> int:

@@ -105,6 +105,24 @@ def test_stage1_kernel_selection():
     assert rows(4096, prox.INT4, 128, 16, 4097) == 0
 
 
+def test_stage2_kernel_selection():
+    # More than eight batch rows of 16-bit weights with d_model >= 4096 take
+    # the matrix-core Stage 2 (16 rows per launch); otherwise the VALU kernel
+    # (8 rows per launch, fewer for INT4 weights at wide d_model).
+    rows = prox.stage2_rows
+    assert rows(4096, 14336, False, 16) == 16
+    assert rows(4096, 14336, False, 9) == 16
+    assert rows(4096, 14336, False, 8) == 8
+    assert rows(8192, 28672, False, 64) == 16
+    assert rows(16384, 320, False, 12) == 16
+    assert rows(2048, 3000, False, 16) == 8         # narrow d: VALU kernel
+    assert rows(8192, 28672, True, 16) == 4         # INT4 weights: x rows in LDS
+    assert rows(16384, 320, True, 16) == 2
+    assert rows(4096, 14336, False, 65) == 0        # batch
+    assert rows(4096, 14336, False, 0) == 0
+    assert rows(4000, 14336, False, 16) == 0        # d_model % 128
+
+
 def test_sparse_rejects_bad_arguments():
     L = prox.lib()
     assert _sparse(k_in=0) == INVALID

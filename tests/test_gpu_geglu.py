@@ -18,6 +18,8 @@ CASES = {
                                               qbits=8, group=512),
     "bf16_i4_geglu_2048x3000_b4": W.small_config(d=2048, f=3000, batch=4, seed=43, sigma_w=0.02),
     "bf16_i4_geglu_256x640_b16": W.small_config(d=256, f=640, batch=16, seed=44),
+    "bf16_i4_geglu_4096x900_b16": W.small_config(d=4096, f=900, batch=16, seed=45,
+                                                 sigma_w=0.02),
 }
 
 

@@ -140,14 +140,15 @@ size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
 int prox_stage1_mfma_rows(int d_model, prox_qfmt fmt, int group, int batch, int k_in);
 
 /*
- * Which Stage-2 kernel a call takes (for inspection and tests): the batch rows
- * one Stage-2 launch covers.  16 means the matrix-core kernel (more than eight
- * batch rows of 16-bit weights with d_model >= 4096: gate/up as 16x16x16
- * MFMAs, the three matrices read once per 16 rows); otherwise the VALU kernel
- * takes up to 8 rows per launch (fewer for INT4 weights, w4 != 0, at wide
- * d_model), and a batch tail of 8 rows or fewer always runs on it.  0 for an
- * unsupported shape or batch.  Host only, no HIP calls.  Both kernels give
- * the same kept set; y differs only in fp32 summation order.
+ * Which Stage-2 path a call takes (for inspection and tests): the batch rows
+ * one Stage-2 pass covers.  16 means the matrix-core path (more than eight
+ * batch rows of 16-bit weights with d_model >= 4096): every chunk of up to 16
+ * rows, the batch tail included, runs gate/up as 16x16x16 MFMAs and then the
+ * down projection as a second launch, so the three matrices are read once per
+ * 16 rows.  Otherwise one fused VALU launch per up to 8 rows (fewer for INT4
+ * weights, w4 != 0, at wide d_model).  0 for an unsupported shape or batch.
+ * Host only, no HIP calls.  Both paths give the same kept set; y differs only
+ * in fp32 summation order.
  */
 int prox_stage2_rows(int d_model, int d_ff, int w4, int batch);
 

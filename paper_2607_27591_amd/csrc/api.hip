@@ -81,7 +81,7 @@ prox_status hip_status(hipError_t e) { return e == hipSuccess ? PROX_OK : PROX_E
     } while (0)
 
 struct Ws {
-    float *scores, *ypart;
+    float *scores, *ypart, *sbuf;
     int32_t *klist;
 };
 
@@ -92,6 +92,7 @@ Ws carve(void *ws, int d, int f, int batch) {
     w.scores = reinterpret_cast<float *>(b + L.scores);
     w.ypart = reinterpret_cast<float *>(b + L.ypart);
     w.klist = reinterpret_cast<int32_t *>(b + L.klist);
+    w.sbuf = reinterpret_cast<float *>(b + L.sbuf);
     return w;
 }
 
@@ -114,24 +115,39 @@ prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff
     // grid for every channel (workgroups past the count get no channels).
     const int nwg = stage2_wgs(scores && !sel.tau_mode ? k_ff : f);
     const int ystride = ypart_rows(batch);
-    // More than eight rows of 16-bit weights: the matrix-core kernel, up to
-    // 16 rows per launch (a tail of eight or fewer rows takes the VALU kernel).
+    // More than eight rows of 16-bit weights: the matrix-core path, 16 rows
+    // per chunk (its tail too).
     const int rows = stage2_launch_rows(d, m.s2.wq, batch);
+    if (rows == kStage2MfmaRows) {
+        // Every 16-row chunk: gate/up on the matrix cores (s to the
+        // workspace, kept list written by the first chunk), then the down
+        // projection over kStage2DownGroups channel groups; the reduction
+        // sums those groups' partial y.
+        const int n_max = scores && !sel.tau_mode ? k_ff : f;
+        for (int c0 = 0; c0 < batch; c0 += rows) {
+            const int nb = batch - c0 < rows ? batch - c0 : rows;
+            const int list_mode = !scores ? kListNone : c0 == 0 ? kListWrite : kListRead;
+            PROX_TRY(launch_stage2_mfma(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff,
+                                        mask, c0 == 0 ? scores_copy : nullptr, W.sbuf, nwg,
+                                        c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr},
+                                        m.act, W.klist, list_mode, stream));
+            PROX_TRY(launch_stage2_down(dt, nb, d, f, m.s2.wd, W.sbuf, scores ? W.klist : nullptr,
+                                        n_max, W.ypart + (size_t)c0 * d, ystride, stream));
+        }
+        if (events) PROX_TRY(hipEventRecord(events[2], stream));
+        PROX_TRY(launch_reduce(dt, W.ypart, kStage2DownGroups, batch, d, y, stream));
+        if (events) PROX_TRY(hipEventRecord(events[3], stream));
+        return PROX_OK;
+    }
     for (int c0 = 0; c0 < batch; c0 += rows) {
         const int nb = batch - c0 < rows ? batch - c0 : rows;
         const int list_mode = !scores || rows >= batch ? kListNone
                               : c0 == 0             ? kListWrite
                                                     : kListRead;
-        const Select sl = c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr};
-        float *const sc = c0 == 0 ? scores_copy : nullptr;
-        if (nb > kStage2MaxNB)
-            PROX_TRY(launch_stage2_mfma(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff,
-                                        mask, sc, W.ypart + (size_t)c0 * d, ystride, nwg, sl,
-                                        m.act, W.klist, list_mode, stream));
-        else
-            PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
-                                   sc, W.ypart + (size_t)c0 * d, ystride, nwg, sl, m.act,
-                                   W.klist, list_mode, stream));
+        PROX_TRY(launch_stage2(dt, xb + (size_t)c0 * d, nb, d, f, m.s2, scores, k_ff, mask,
+                               c0 == 0 ? scores_copy : nullptr, W.ypart + (size_t)c0 * d, ystride,
+                               nwg, c0 == 0 ? sel : Select{sel.tau_mode, sel.tau, nullptr}, m.act,
+                               W.klist, list_mode, stream));
     }
     if (events) PROX_TRY(hipEventRecord(events[2], stream));
     PROX_TRY(launch_reduce(dt, W.ypart, nwg, batch, d, y, stream));

@@ -63,14 +63,22 @@ hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const S
                          const float *scores, int k_ff, uint8_t *mask, float *scores_copy,
                          float *ypart, int ystride, int nwg, Select sel, int act,
                          int32_t *klist, int klist_mode, hipStream_t stream);
-// The same Stage 2 for 9 to kStage2MfmaRows batch rows in one launch, with
-// gate/up on the matrix cores; 16-bit weights and d >= 4096 only
-// (stage2_mfma_ok).  Same arguments, workspace layout and kept-list modes.
+// Stage 2 for up to kStage2MfmaRows batch rows (16-bit weights, d >= 4096:
+// stage2_mfma_ok) in two launches.  launch_stage2_mfma selects like
+// launch_stage2 (same kept-list modes; the sparse path must write or read
+// klist, since the down launch takes the kept channels from it), runs gate/up
+// on the matrix cores and writes s of kept-list position p and batch row b to
+// sbuf[p * kStage2MfmaRows + b].  launch_stage2_down then splits the kept
+// list (klist, or every channel when klist is NULL) into kStage2DownGroups
+// groups and writes the partial y of group g to ypart[(g * ystride + b) * d +
+// c]; n_max bounds the kept count (k_ff, or f).
 bool stage2_mfma_ok(int d, int wq);
 hipError_t launch_stage2_mfma(int dtype, const void *x, int nb, int d, int f,
                               const Stage2Weights &w, const float *scores, int k_ff,
-                              uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                              int nwg, Select sel, int act, int32_t *klist, int klist_mode,
+                              uint8_t *mask, float *scores_copy, float *sbuf, int nwg, Select sel,
+                              int act, int32_t *klist, int klist_mode, hipStream_t stream);
+hipError_t launch_stage2_down(int dtype, int nb, int d, int f, const void *wd, const float *sbuf,
+                              const int32_t *klist, int n_max, float *ypart, int ystride,
                               hipStream_t stream);
 // INT4 base weights: quantise W_gate, W_up, W_down (channel-major [f][d]) into
 // a W4Layout blob, and the inverse view of matrix m (0 gate, 1 up, 2 down).

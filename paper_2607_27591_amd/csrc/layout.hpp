@@ -107,6 +107,7 @@ struct W4Layout {
 
 constexpr int kStage2MaxNB = 8;          // batch rows per Stage 2 launch
 constexpr int kStage2MfmaRows = 16;      // ... of the matrix-core Stage 2 (16-bit weights)
+constexpr int kStage2DownGroups = 64;    // kept-channel groups of its down projection
 
 // Batch rows a Stage 2 launch of nb <= 8 rows is compiled for (1, 2, 4 or 8).
 __host__ __device__ inline int stage2_nb_t(int nb) {
@@ -132,15 +133,18 @@ struct Select {
 // Workspace (no initialisation needed)
 // ---------------------------------------------------------------------------
 // scores: the proxy scores (fp32, f padded to 128); ypart: per-workgroup
-// partial y rows of Stage 2.
+// partial y rows of Stage 2; sbuf (more than kStage2MaxNB rows only): s of
+// the kept channels in kept-list order, [f][kStage2MfmaRows] fp32.
 struct WsLayout {
-    size_t scores, klist, ypart, total;
+    size_t scores, klist, ypart, sbuf, total;
     __host__ __device__ WsLayout(int d, int f, int batch) {
         const int f_pad = (f + 127) / 128 * 128;
         size_t o = 0;
         scores = o; o = align_up(o + (size_t)f_pad * 4, 256);
         klist = o; o = align_up(o + (size_t)(f + 1) * 4, 256);   // kept channels, then their count
         ypart = o; o = align_up(o + (size_t)kStage2MaxWGs * ypart_rows(batch) * d * 4, 256);
+        sbuf = o;
+        if (batch > kStage2MaxNB) o = align_up(o + (size_t)f * kStage2MfmaRows * 4, 256);
         total = o;
     }
 };

@@ -63,7 +63,8 @@ struct Stage2Smem {
 };
 
 // The selection prologue of both Stage 2 kernels: this workgroup's slice of the
-// kept channels (their ids to list[0..n), n returned) and its chunk of the mask.
+// kept channels (their ids to list[0..n), n returned, the slice's first
+// kept-list position to p0_out) and its chunk of the mask.
 // Every workgroup ranks the scores itself (top-k or the threshold rule), or,
 // for the later launches of a multi-launch batch, reads the first launch's list.
 // The caller synchronises before reading list.
@@ -72,7 +73,8 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
                                             uint8_t *__restrict__ mask,
                                             float *__restrict__ scores_copy, Select sel_rule,
                                             int32_t *__restrict__ klist, int klist_mode,
-                                            TopKScratch &tk, TopKOrder<C> &ord, int *list) {
+                                            TopKScratch &tk, TopKOrder<C> &ord, int *list,
+                                            int &p0_out) {
     const int tid = threadIdx.x;
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
@@ -143,7 +145,7 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
     } else {
         for (int t = tid; t < n; t += kBlock) list[t] = p0 + t;
     }
-
+    p0_out = p0;
     return n;
 }
 
@@ -167,8 +169,10 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     __shared__ Stage2Smem sm;
     extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
 
+    int p0;
     const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
-                                  klist_mode, tk, ord, sm.list);
+                                  klist_mode, tk, ord, sm.list, p0);
+    (void)p0;
 
     const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
     uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
@@ -488,8 +492,9 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// stage2_mfma_kernel: Stage 2 for 9 to 16 batch rows of 16-bit weights in one
-// launch, so every kept row of the three matrices is read once for all rows.
+// stage2_mfma_kernel + stage2_down_kernel: Stage 2 for up to 16 batch rows of
+// 16-bit weights, so every kept row of the three matrices is read once for
+// all of them.
 //  prologue  the slice of kept channels, as in stage2_kernel.
 //  gate/up   on the matrix cores: the slice is cut into tiles of 16 channels,
 //            and wave w takes the w-th sixteenth of d for every tile, so the
@@ -498,16 +503,20 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
 //            of each matrix (A) and of one batch row of x (B, from L2), and two
 //            16 x 16 x 16 MFMAs per matrix add the products into the tile's
 //            [16 channels][16 rows] fp32 sums.  The 16 waves' sums of a tile
-//            are added through LDS in wave order; s = act(g) u goes to LDS.
-//  down      VALU: every thread owns 4 output columns and all 16 rows.
+//            are added through LDS in wave order; s = act(g) u goes to the
+//            workspace at the channel's kept-list position.
+//  down      a second launch: the kept list is cut into kStage2DownGroups
+//            groups, and each workgroup takes one group and 1024 columns,
+//            with the group's s in LDS; every thread owns 4 columns and all 16
+//            rows (VALU), and four thread groups split the channels.  With 64 groups the partial y are a quarter of
+//            what one partial per Stage 2 workgroup would be: at 16 rows those
+//            are as large as the weights the step reads.
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kS2mTiles = 2;   // channel tiles per pass through the gate/up loop
 constexpr int kS2mRed = kS2mTiles * 2 * kMaxBlockWaves * kWave;   // float4 per pass
 
-size_t stage2_mfma_lds_bytes() {
-    return (size_t)kS2mRed * 16 + (size_t)kMaxSlice * kStage2MfmaRows * 4;
-}
+size_t stage2_mfma_lds_bytes() { return (size_t)kS2mRed * 16; }
 
 bool stage2_mfma_ok(int d, int wq) { return wq == 16 && d >= 4 * kBlock; }
 
@@ -515,23 +524,22 @@ template <int DT, int C>
 __global__ __launch_bounds__(kBlock) void stage2_mfma_kernel(
     const uint16_t *__restrict__ x, int nb, int d, int f, Stage2Weights wt,
     const float *__restrict__ scores, int k_ff, uint8_t *__restrict__ mask,
-    float *__restrict__ scores_copy, float *__restrict__ ypart, int ypart_stride,
-    Select sel_rule, int act, int32_t *__restrict__ klist, int klist_mode) {
+    float *__restrict__ scores_copy, float *__restrict__ sbuf, Select sel_rule, int act,
+    int32_t *__restrict__ klist, int klist_mode) {
     constexpr int R = kStage2MfmaRows;
     const uint16_t *__restrict__ wg = static_cast<const uint16_t *>(wt.wg);
     const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
-    const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
 
     __shared__ TopKScratch tk;
     __shared__ TopKOrder<C> ord;
     __shared__ int list[kMaxSlice];
-    extern __shared__ __align__(16) float dyn[];   // red [tiles][2][waves][lanes] float4 | s [slice][R]
+    extern __shared__ __align__(16) float dyn[];   // red [tiles][2][waves][lanes] float4
     float4 *red = reinterpret_cast<float4 *>(dyn);
-    float *s_sh = dyn + (size_t)kS2mRed * 4;
 
+    int p0;
     const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
-                                  klist_mode, tk, ord, list);
+                                  klist_mode, tk, ord, list, p0);
     __syncthreads();
 
     // ---- gate/up ----
@@ -602,51 +610,101 @@ __global__ __launch_bounds__(kBlock) void stage2_mfma_kernel(
                 us += rf[(((tt * 2 + 1) * kMaxBlockWaves + w) * kWave + ln) * 4 + e];
             }
             const int t = (t0 + tt) * 16 + 4 * (ln / 16) + e;
-            if (t < n) s_sh[t * R + ln % 16] = gate_act(gs, act) * us;
+            if (t < n) sbuf[(size_t)(p0 + t) * R + ln % 16] = gate_act(gs, act) * us;
         }
         __syncthreads();
     }
+}
 
-    // ---- down: partial y over this slice, 4 columns x 16 rows per thread ----
-    constexpr int UD = 8;
-    for (int cg = tid; cg < d / 4; cg += kBlock) {
-        float acc[R][4];
+constexpr int kDownCols = 256;              // 4-column groups per workgroup: 1024 columns
+constexpr int kDownSplit = kBlock / kDownCols;   // thread groups splitting its channels
+
+size_t stage2_down_lds_bytes(int n_max) {
+    const size_t m = (size_t)(n_max + kStage2DownGroups - 1) / kStage2DownGroups;
+    return (size_t)kStage2MfmaRows * kDownCols * 16 + m * (kStage2MfmaRows * 4 + 4);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kBlock) void stage2_down_kernel(
+    int nb, int d, int f, const uint16_t *__restrict__ wd, const float *__restrict__ sbuf,
+    const int32_t *__restrict__ klist, float *__restrict__ ypart, int ypart_stride) {
+    constexpr int R = kStage2MfmaRows;
+    extern __shared__ __align__(16) float dyn[];   // red [R][kDownCols] float4 | s [m][R] | ids [m]
+    const int tid = threadIdx.x;
+    const int n_ch = klist ? klist[f] : f;
+    const int grp = blockIdx.y;
+    const int q0 = (int)((long long)grp * n_ch / kStage2DownGroups);
+    const int m = (int)((long long)(grp + 1) * n_ch / kStage2DownGroups) - q0;
+    float4 *red = reinterpret_cast<float4 *>(dyn);
+    float *s_l = dyn + (size_t)R * kDownCols * 4;
+    int *ids = reinterpret_cast<int *>(s_l + (size_t)m * R);
+    for (int e = tid; e < m * R; e += kBlock) s_l[e] = sbuf[(size_t)q0 * R + e];
+    for (int t = tid; t < m; t += kBlock) ids[t] = klist ? klist[q0 + t] : q0 + t;
+    __syncthreads();
+
+    // Thread group sub takes channels sub, sub + kDownSplit, ... of the group.
+    const int sub = tid / kDownCols, cgl = tid % kDownCols;
+    const int cg = blockIdx.x * kDownCols + cgl;   // columns 4 cg .. 4 cg + 3
+    const bool active = cg < d / 4;
+    constexpr int UD = 12;   // rows in flight
+    float acc[R][4];
 #pragma unroll
-        for (int b = 0; b < R; ++b)
+    for (int b = 0; b < R; ++b)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
-        for (int t0 = 0; t0 < n; t0 += UD) {
+        for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
+    if (active) {
+        for (int t0 = sub; t0 < m; t0 += kDownSplit * UD) {
             uint2 wv[UD];
 #pragma unroll
             for (int u = 0; u < UD; ++u) {
-                const int t = t0 + u;
-                if (t < n) {
+                const int t = t0 + u * kDownSplit;
+                if (t < m) {
                     const u32x2 v = __builtin_nontemporal_load(
-                        reinterpret_cast<const u32x2 *>(wd + (size_t)list[t] * d + cg * 4));
+                        reinterpret_cast<const u32x2 *>(wd + (size_t)ids[t] * d + cg * 4));
                     wv[u] = make_uint2(v.x, v.y);
                 }
             }
 #pragma unroll
             for (int u = 0; u < UD; ++u) {
-                const int t = t0 + u;
-                if (t < n) {
+                const int t = t0 + u * kDownSplit;
+                if (t < m) {
                     const float wf[4] = {lo_to_float<DT>(wv[u].x), hi_to_float<DT>(wv[u].x),
                                          lo_to_float<DT>(wv[u].y), hi_to_float<DT>(wv[u].y)};
 #pragma unroll
                     for (int b = 0; b < R; ++b) {
-                        const float sv = s_sh[t * R + b];
+                        const float sv = s_l[t * R + b];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
                     }
                 }
             }
         }
+    }
+    // The thread groups' sums are added in group order through LDS; every
+    // thread reaches every barrier.
+    for (int g2 = 0; g2 < kDownSplit - 1; ++g2) {
+        if (sub == g2) {
+#pragma unroll
+            for (int b = 0; b < R; ++b) {
+                float4 v = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+                if (g2 > 0) {
+                    const float4 o = red[b * kDownCols + cgl];
+                    v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+                }
+                red[b * kDownCols + cgl] = v;
+            }
+        }
+        __syncthreads();
+    }
+    if (sub == kDownSplit - 1 && active) {
 #pragma unroll
         for (int b = 0; b < R; ++b) {
             if (b < nb) {
+                const float4 o = red[b * kDownCols + cgl];
                 float4 *dst = reinterpret_cast<float4 *>(
-                    ypart + ((size_t)blockIdx.x * ypart_stride + b) * d + cg * 4);
-                *dst = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+                    ypart + ((size_t)grp * ypart_stride + b) * d + cg * 4);
+                *dst = make_float4(o.x + acc[b][0], o.y + acc[b][1], o.z + acc[b][2],
+                                   o.w + acc[b][3]);
             }
         }
     }
@@ -802,25 +860,23 @@ hipError_t launch_stage2(int dtype, const void *x, int nb, int d, int f, const S
 template <int DT, int C>
 static hipError_t launch_stage2m_t(const void *x, int nb, int d, int f, const Stage2Weights &wt,
                                    const float *scores, int k_ff, uint8_t *mask,
-                                   float *scores_copy, float *ypart, int ystride, int nwg,
-                                   Select sel_rule, int act, int32_t *klist, int klist_mode,
-                                   hipStream_t st) {
+                                   float *scores_copy, float *sbuf, int nwg, Select sel_rule,
+                                   int act, int32_t *klist, int klist_mode, hipStream_t st) {
     const size_t lds = stage2_mfma_lds_bytes();
     hipError_t e = allow_lds(stage2_mfma_kernel<DT, C>, lds);
     if (e != hipSuccess) return e;
     stage2_mfma_kernel<DT, C><<<nwg, kBlock, lds, st>>>(
-        static_cast<const uint16_t *>(x), nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
-        ystride, sel_rule, act, klist, klist_mode);
+        static_cast<const uint16_t *>(x), nb, d, f, wt, scores, k_ff, mask, scores_copy, sbuf,
+        sel_rule, act, klist, klist_mode);
     return hipGetLastError();
 }
 
 template <int DT>
 static hipError_t launch_stage2m_c(const void *x, int nb, int d, int f, const Stage2Weights &wt,
                                    const float *scores, int k_ff, uint8_t *mask,
-                                   float *scores_copy, float *ypart, int ystride, int nwg,
-                                   Select sel_rule, int act, int32_t *klist, int klist_mode,
-                                   hipStream_t st) {
-#define S2M(C_) launch_stage2m_t<DT, C_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart, ystride, nwg, sel_rule, act, klist, klist_mode, st)
+                                   float *scores_copy, float *sbuf, int nwg, Select sel_rule,
+                                   int act, int32_t *klist, int klist_mode, hipStream_t st) {
+#define S2M(C_) launch_stage2m_t<DT, C_>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, sbuf, nwg, sel_rule, act, klist, klist_mode, st)
     if (scores && f <= 4 * kBlock) return S2M(4);
     if (scores && f <= 8 * kBlock) return S2M(8);
     if (scores && f <= 12 * kBlock) return S2M(12);
@@ -833,19 +889,44 @@ static hipError_t launch_stage2m_c(const void *x, int nb, int d, int f, const St
 
 hipError_t launch_stage2_mfma(int dtype, const void *x, int nb, int d, int f,
                               const Stage2Weights &wt, const float *scores, int k_ff,
-                              uint8_t *mask, float *scores_copy, float *ypart, int ystride,
-                              int nwg, Select sel_rule, int act, int32_t *klist, int klist_mode,
+                              uint8_t *mask, float *scores_copy, float *sbuf, int nwg,
+                              Select sel_rule, int act, int32_t *klist, int klist_mode,
                               hipStream_t st) {
     const int n_ch = scores && !sel_rule.tau_mode ? k_ff : f;   // the kept-list length
     if (nb < 1 || nb > kStage2MfmaRows || !stage2_mfma_ok(d, wt.wq) || nwg < 1 ||
-        nwg > kStage2MaxWGs || (long long)n_ch > (long long)kMaxSlice * nwg)
+        nwg > kStage2MaxWGs || (long long)n_ch > (long long)kMaxSlice * nwg || !sbuf)
         return hipErrorInvalidValue;
-    if (klist_mode != kListNone && (!scores || !klist)) return hipErrorInvalidValue;
+    // The down launch reads the kept list: a sparse call writes or reads it.
+    if ((scores != nullptr) != (klist_mode != kListNone) || (scores && !klist))
+        return hipErrorInvalidValue;
     if (dtype == kBF16)
-        return launch_stage2m_c<kBF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
-                                       ystride, nwg, sel_rule, act, klist, klist_mode, st);
-    return launch_stage2m_c<kF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, ypart,
-                                  ystride, nwg, sel_rule, act, klist, klist_mode, st);
+        return launch_stage2m_c<kBF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, sbuf,
+                                       nwg, sel_rule, act, klist, klist_mode, st);
+    return launch_stage2m_c<kF16>(x, nb, d, f, wt, scores, k_ff, mask, scores_copy, sbuf, nwg,
+                                  sel_rule, act, klist, klist_mode, st);
+}
+
+hipError_t launch_stage2_down(int dtype, int nb, int d, int f, const void *wd, const float *sbuf,
+                              const int32_t *klist, int n_max, float *ypart, int ystride,
+                              hipStream_t st) {
+    if (nb < 1 || nb > kStage2MfmaRows || d % 4 != 0 || n_max < 0 || n_max > f || !sbuf ||
+        (!klist && n_max != f))
+        return hipErrorInvalidValue;
+    const size_t lds = stage2_down_lds_bytes(n_max);
+    const dim3 grid((d / 4 + kDownCols - 1) / kDownCols, kStage2DownGroups);
+    const uint16_t *w = static_cast<const uint16_t *>(wd);
+    if (dtype == kBF16) {
+        hipError_t e = allow_lds(stage2_down_kernel<kBF16>, lds);
+        if (e != hipSuccess) return e;
+        stage2_down_kernel<kBF16><<<grid, kBlock, lds, st>>>(nb, d, f, w, sbuf, klist, ypart,
+                                                                   ystride);
+    } else {
+        hipError_t e = allow_lds(stage2_down_kernel<kF16>, lds);
+        if (e != hipSuccess) return e;
+        stage2_down_kernel<kF16><<<grid, kBlock, lds, st>>>(nb, d, f, w, sbuf, klist, ypart,
+                                                                  ystride);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, void *y,

@@ -46,8 +46,8 @@ SMALL = {
     "bf16_i4_16384x320_b6": W.small_config(d=16384, f=320, batch=6, seed=15, in_frac=0.3,
                                            sigma_w=0.01),
     # More than eight rows of 16-bit weights at d_model >= 4096 run Stage 2 on
-    # the matrix cores: 9 fp16 rows in one launch, and 33 rows as two 16-row
-    # launches and a 1-row VALU launch sharing one kept list.
+    # the matrix cores: 9 fp16 rows in one chunk, and 33 rows as chunks of 16,
+    # 16 and 1 sharing one kept list.
     "f16_i4_4096x1000_b9": W.small_config(d=4096, f=1000, batch=9, seed=18, dtype=W.DT_F16,
                                           in_frac=0.5, sigma_w=0.02),
     "bf16_i4_8192x700_b33": W.small_config(d=8192, f=700, batch=33, seed=19, in_frac=0.4,

@@ -48,6 +48,31 @@ def test_c4_8192x28672_bf16():
     _full("c4_8192x28672_bf16", 3)
 
 
+def test_max_dff_matrix_core_stage2():
+    """d_ff 65536 with 9 batch rows on the matrix-core Stage 2: 64 score keys
+    per thread in its selection, 1024 channels per down group (the down
+    kernel's largest LDS), and the dense FFN over every channel; full keep
+    equals dense bitwise."""
+    cfg = W.small_config(d=4096, f=65536, batch=9, seed=20, in_frac=0.5, ff_frac=0.2,
+                         sigma_w=0.02)
+    assert prox.stage2_rows(cfg.d_model, cfg.d_ff, False, cfg.batch) == 16
+    log("[full] 4096x65536 b9: generating and packing")
+    case = make_case(cfg)
+    x = case.wl.x_vectors(1, cfg.batch)[0]
+    out = run_sparse(case, x, cfg.k_in, cfg.k_ff)
+    log(f"    {check_sparse(case, x, cfg.k_in, cfg.k_ff, out, tag='4096x65536 b9')}")
+    y = prox.to_bits(prox.ffn_dense(case.w, prox.from_bits(x, cfg.dtype)))
+    torch.cuda.synchronize()
+    ref = oracle.ffn_dense(x, cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down)
+    err = y_rel_err(y, ref, cfg.dtype)
+    log(f"    dense y err {err:.3e}")
+    assert err <= Y_TOL
+    full = run_sparse(case, x, cfg.d_model, cfg.d_ff)
+    assert full.mask.all() and np.array_equal(full.y, y)
+    del case
+    torch.cuda.empty_cache()
+
+
 @pytest.fixture(scope="module")
 def c3_case():
     cfg = W.CONFIGS["c3_4096x14336_bf16"]

@@ -719,23 +719,27 @@ constexpr int kReduceThreads = 256;
 constexpr int kReduceCols = 32;
 constexpr int kReduceGroups = kReduceThreads / kReduceCols;                 // 8
 constexpr int kReducePerThread = (kStage2MaxWGs + kReduceGroups - 1) / kReduceGroups;   // 32
+constexpr int kReduceSmall = kStage2DownGroups / kReduceGroups;   // 8: for <= 64 partials
 
-template <int DT>
+// UPT: partials per thread (kReducePerThread, or kReduceSmall when nwg <= 64,
+// which adds the same terms in the same order).
+
+template <int DT, int UPT>
 __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const float *__restrict__ ypart, int nwg,
                                                                 int nbt, int d, uint16_t *__restrict__ y) {
     __shared__ float red[kReduceGroups][kReduceCols];
     const int b = blockIdx.y, col = threadIdx.x % kReduceCols, g = threadIdx.x / kReduceCols;
     const int c = blockIdx.x * kReduceCols + col;
     const int cc = min(c, d - 1);
-    float v[kReducePerThread];
+    float v[UPT];
 #pragma unroll
-    for (int u = 0; u < kReducePerThread; ++u) {   // clamped loads, masked below
+    for (int u = 0; u < UPT; ++u) {   // clamped loads, masked below
         const int w = min(g + u * kReduceGroups, nwg - 1);
         v[u] = ypart[((size_t)w * nbt + b) * d + cc];
     }
     float acc = 0.0f;
 #pragma unroll
-    for (int u = 0; u < kReducePerThread; ++u)
+    for (int u = 0; u < UPT; ++u)
         if (g + u * kReduceGroups < nwg) acc += v[u];
     red[g][col] = acc;
     __syncthreads();
@@ -933,10 +937,18 @@ hipError_t launch_reduce(int dtype, const float *ypart, int nwg, int nb, int d, 
                          hipStream_t st) {
     dim3 grid((d + kReduceCols - 1) / kReduceCols, nb);
     const int nbt = ypart_rows(nb);
-    if (dtype == kBF16)
-        reduce_kernel<kBF16><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
-    else
-        reduce_kernel<kF16><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, static_cast<uint16_t *>(y));
+    if (nwg < 1 || nwg > kStage2MaxWGs) return hipErrorInvalidValue;
+    uint16_t *yb = static_cast<uint16_t *>(y);
+    if (nwg <= kReduceSmall * kReduceGroups) {
+        if (dtype == kBF16)
+            reduce_kernel<kBF16, kReduceSmall><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, yb);
+        else
+            reduce_kernel<kF16, kReduceSmall><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, yb);
+    } else if (dtype == kBF16) {
+        reduce_kernel<kBF16, kReducePerThread><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, yb);
+    } else {
+        reduce_kernel<kF16, kReducePerThread><<<grid, kReduceThreads, 0, st>>>(ypart, nwg, nbt, d, yb);
+    }
     return hipGetLastError();
 }
 

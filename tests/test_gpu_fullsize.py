@@ -84,7 +84,7 @@ def c3_case():
 
 
 @pytest.mark.parametrize("batch,sparsity", [(1, 0.0), (1, 0.5), (1, 0.7), (1, 0.9), (4, 0.7),
-                                            (4, 0.9), (16, 0.7), (16, 0.0)])
+                                            (4, 0.9), (5, 0.7), (8, 0.7), (16, 0.7), (16, 0.0)])
 def test_c3_batch_sparsity_sweep(c3_case, batch, sparsity):
     cfg = c3_case.cfg
     k_ff = W.frac_to_k(1.0 - sparsity, cfg.d_ff)

@@ -17,6 +17,8 @@
 //            partial y.
 // With INT4 base weights (WQ = 4) the two streaming loops read codes and
 // per-group scales instead of 16-bit rows and dequantise on the fly.
+// stage2_mfma_kernel and stage2_down_kernel (below) take batches of more than
+// 8 rows of 16-bit weights.
 // reduce_kernel sums the partial y of all workgroups in workgroup order and
 // rounds y once.  No floating-point atomics: results are deterministic.
 #include "common.hpp"
@@ -508,9 +510,10 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
 //  down      a second launch: the kept list is cut into kStage2DownGroups
 //            groups, and each workgroup takes one group and 1024 columns,
 //            with the group's s in LDS; every thread owns 4 columns and all 16
-//            rows (VALU), and four thread groups split the channels.  With 64 groups the partial y are a quarter of
-//            what one partial per Stage 2 workgroup would be: at 16 rows those
-//            are as large as the weights the step reads.
+//            rows (VALU), and four thread groups split the channels.  With 64
+//            groups the partial y are a quarter of what one partial per Stage 2
+//            workgroup would be: at 16 rows those are as large as the weights
+//            the step reads.
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kS2mTiles = 2;   // channel tiles per pass through the gate/up loop

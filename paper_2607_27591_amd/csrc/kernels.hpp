@@ -9,6 +9,23 @@
 
 namespace prox {
 
+// Column tile of Stage-1 workgroup b of n.  Workgroups are dealt to the 8 XCDs
+// in turn (XCD b % 8), each with its own L2.  When a row segment of a tile is
+// under 128 bytes (PAIRED: INT4 codes of a 64-column tile), one 128-byte line
+// holds the same kept row of tiles 2p and 2p + 1, so the pair goes to
+// workgroups b and b + 8 of one XCD and its L2 fetches the line once.  The
+// last n % 16 workgroups keep tile b.  A bijection of [0, n).
+template <bool PAIRED>
+__device__ __forceinline__ int stage1_tile(int b, int n) {
+    if constexpr (!PAIRED) {
+        return b;
+    } else {
+        if (b >= (n & ~15)) return b;
+        const int x = b & 7, q = b >> 3;
+        return 2 * ((q >> 1) * 8 + x) + (q & 1);
+    }
+}
+
 hipError_t launch_pack(int dtype, int qbits, const void *wg, const void *wu, int d, int f,
                        int group, void *blob, hipStream_t stream);
 hipError_t launch_unpack(int qbits, const void *blob, int d, int f, int group, int8_t *cg,

@@ -146,7 +146,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     using W = typename ProxyLoad<QB, CPL>::type;
     const BlobLayout L(d, f, QB, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
-    const int tile = blockIdx.x;
+    const int tile = stage1_tile<2 * T * QB / 8 < 128>(blockIdx.x, gridDim.x);
     const int ng = d / group;
 
     __shared__ TopKScratch tk;

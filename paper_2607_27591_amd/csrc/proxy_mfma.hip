@@ -66,7 +66,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     constexpr float off = Int4Magic<DT>::offset;
     const BlobLayout L(d, f, 4, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
-    const int tile = blockIdx.x;
+    const int tile = stage1_tile<T == 64>(blockIdx.x, gridDim.x);   // INT4 codes
     const int ng = d / group;
 
     __shared__ TopKScratch tk;

@@ -55,11 +55,12 @@ typedef enum { PROX_ACT_SILU = 0, PROX_ACT_GELU = 1 } prox_act;
 typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1, PROX_Q_NONE = 2 } prox_qfmt;
 
 /* Supported sizes.  Batches past the rows one launch takes (Stage 1: 4 on the
- * dot-product kernel, 8 or 16 on the matrix cores; Stage 2: 8, fewer for INT4
- * base weights on wide d_model) run as several launches on the same stream:
+ * dot-product kernel, 8 or 16 on the matrix cores; Stage 2: 16 per chunk on
+ * the matrix-core path, see prox_stage2_rows, else 8, fewer for INT4 base
+ * weights on wide d_model) run as several launches on the same stream:
  * Stage 1 takes the max of the scores over them, Stage 2 writes disjoint rows
  * of the partial sums, so the result does not depend on the split.  Each
- * Stage 2 launch reads the kept rows again. */
+ * Stage 2 launch or chunk reads the kept rows again. */
 #define PROX_MAX_BATCH 64
 #define PROX_MIN_D_MODEL 128
 #define PROX_MAX_D_MODEL 16384   /* multiple of 128 */

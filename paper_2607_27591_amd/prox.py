@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libprox.so")
 
 F16, BF16 = 0, 1
 INT8, INT4, NONE = 0, 1, 2   # NONE: unquantised 16-bit proxy (group = d_model)
-MAX_BATCH = 16
+MAX_BATCH = 64   # PROX_MAX_BATCH of include/prox.h
 SPARSE_STAGES = 3
 
 _TORCH_DT = {torch.float16: F16, torch.bfloat16: BF16}

@@ -43,6 +43,12 @@ def test_library_exports_every_declared_symbol():
     assert set(_declared()) <= exported
 
 
+def test_binding_constants_match_the_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define PROX_MAX_BATCH\s+(\d+)", text).group(1)) == prox.MAX_BATCH
+    assert int(re.search(r"#define PROX_SPARSE_STAGES\s+(\d+)", text).group(1)) == prox.SPARSE_STAGES
+
+
 def test_library_is_gfx950_only():
     out = subprocess.run(["strings", prox.LIB_PATH], capture_output=True, text=True).stdout
     assert "gfx950" in out

@@ -58,3 +58,30 @@ def test_allocation_rejects_bad_arguments():
     assert L.prox_allocate_sparsity(float("nan"), 1 / 3, 0.7, 0, 0.7, ctypes.byref(a),
                                     ctypes.byref(b)) == 1
     assert L.prox_allocate_sparsity(0.5, 1 / 3, 0.7, 0.0, 0.7, None, ctypes.byref(b)) == 1
+
+
+@pytest.mark.parametrize("row", GOLDEN["cap_sensitivity"],
+                         ids=lambda r: f"cap{r['s1_max']}_e{r['e']}")
+def test_stage1_cap_rows_reproduce_printed_table(oracle_lib, row):
+    """Every row of the cap-sensitivity table is an active cap: s1 sits at the
+    cap and s2 is re-solved from the cost model to the printed value."""
+    s1, s2 = oracle_lib.allocate(row["e"], s1_max=row["s1_max"])
+    assert s1 == pytest.approx(row["s1_max"], abs=1e-15)
+    assert abs(s2 - row["s2"]) < 5e-4
+    assert oracle_lib.effective_sparsity(s1, s2) == pytest.approx(row["e"], abs=1e-12)
+    assert prox.allocate_sparsity(row["e"], s1_max=row["s1_max"]) == pytest.approx(
+        (s1, s2), abs=1e-12)
+
+
+def test_stage1_cap_only_binds_at_high_sparsity(oracle_lib):
+    """The table's text: at e = 40% and 50% every tested cap leaves the
+    unconstrained allocation alone; at 60% only the 50% cap changes it."""
+    unconstrained = {e: oracle_lib.allocate(e, s1_max=1.0) for e in (0.4, 0.5, 0.6)}
+    for cap in GOLDEN["cap_tested"]:
+        for e in (0.4, 0.5):
+            assert oracle_lib.allocate(e, s1_max=cap) == unconstrained[e]
+        changed = oracle_lib.allocate(0.6, s1_max=cap) != unconstrained[0.6]
+        assert changed == (cap < 0.55)
+        for e in (0.4, 0.5, 0.6):
+            assert prox.allocate_sparsity(e, s1_max=cap) == pytest.approx(
+                oracle_lib.allocate(e, s1_max=cap), abs=1e-12)

@@ -42,22 +42,78 @@ def _tiny(seed=5, d=64, f=96, B=1, dtype=W.DT_BF16, sigma=0.05, x_kind="laplace"
 # ---------------------------------------------------------------------------
 
 def test_half_to_double_exhaustive(oracle_lib):
+    """All 65536 patterns of both formats against numpy's fp16 and the bf16
+    definition (the top half of a binary32)."""
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     want16 = bits.view(np.float16).astype(np.float64)
     with np.errstate(invalid="ignore"):
         wantbf = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    rng = np.random.default_rng(0)
-    for b in rng.choice(65536, 4000, replace=False):
-        got16 = oracle_lib.half_to_double(int(b), W.DT_F16)
-        gotbf = oracle_lib.half_to_double(int(b), W.DT_BF16)
-        if np.isnan(want16[b]):
-            assert math.isnan(got16)
-        else:
-            assert got16 == want16[b]
-        if np.isnan(wantbf[b]):
-            assert math.isnan(gotbf)
-        else:
-            assert gotbf == wantbf[b]
+    for dt, want in ((W.DT_F16, want16), (W.DT_BF16, wantbf)):
+        got = oracle_lib.halves_to_double(bits, dt)
+        nan = np.isnan(want)
+        assert np.array_equal(np.isnan(got), nan)
+        assert np.array_equal(got[~nan], want[~nan])
+        # the scalar entry point agrees with the array one on a spread of patterns
+        for b in range(0, 65536, 257):
+            g = oracle_lib.half_to_double(b, dt)
+            assert (math.isnan(g) and nan[b]) or g == want[b]
+
+
+def _bf16_rne_exact(v):
+    """bfloat16 RNE of a finite double by exact rational arithmetic (bit
+    pattern): the quantum of the value's binade (2^-133 below 2^-126), the
+    quotient rounded half to even, overflow to infinity at 2^128."""
+    from fractions import Fraction
+    sign = 0x8000 if math.copysign(1.0, v) < 0 else 0
+    a = Fraction(abs(v))
+    if a == 0:
+        return sign
+    e = math.frexp(abs(v))[1] - 1
+    e = max(e, -126)
+    quantum = Fraction(2) ** (e - 7)
+    q = a / quantum
+    n = math.floor(q)
+    rem = q - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    r = n * quantum
+    if r >= Fraction(2) ** 128:
+        return sign | 0x7F80
+    f32 = np.array(float(r), np.float32)       # exact: r has at most 8 significant bits
+    assert Fraction(float(f32)) == r
+    return sign | int(f32.view(np.uint32)) >> 16
+
+
+def test_double_to_bf16_is_rne(oracle_lib):
+    """bf16 RNE of the oracle against torch's binary32 -> bfloat16 cast (RNE)
+    on binary32 values, including every 97th midpoint between adjacent bf16
+    values and their binary32 neighbours; and against exact rational rounding
+    on doubles with bits below binary32 precision (where rounding through
+    binary32 first would differ)."""
+    import torch
+    pos = np.arange(0, 0x7F7F, 97, dtype=np.uint32)
+    lo = (pos << 16).view(np.float32).astype(np.float64)
+    hi = ((pos + 1) << 16).view(np.float32).astype(np.float64)
+    mids = ((lo + hi) / 2).astype(np.float32)             # 9 significant bits: exact
+    rng = np.random.default_rng(3)
+    rnd = (rng.standard_normal(4000) * np.exp(rng.uniform(-90, 80, 4000))).astype(np.float32)
+    f32 = np.concatenate([mids, -mids, np.nextafter(mids, np.float32(0)),
+                          np.nextafter(mids, np.float32(np.inf)), rnd,
+                          np.array([0.0, -0.0, 1.0, 3.0e38, 3.4028235e38, 1e-40, 1e-45,
+                                    2.0 ** -126, 2.0 ** -133, 3 * 2.0 ** -134], np.float32)])
+    f32 = f32[np.isfinite(f32)]
+    want = torch.from_numpy(f32.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = oracle_lib.round_to_dtype(f32.astype(np.float64), W.DT_BF16)
+    assert np.array_equal(got, want)
+    for v, w_ in zip(f32[::53], want[::53]):
+        assert oracle_lib.double_to_bf16(float(v)) == int(w_)
+    # doubles that binary32 cannot hold: a midpoint plus or minus 2^-40 of it
+    base = mids[::7].astype(np.float64)
+    near = np.concatenate([base * (1 + 2.0 ** -40), base * (1 - 2.0 ** -40),
+                           rng.standard_normal(500) * np.exp(rng.uniform(-80, 80, 500))])
+    got = oracle_lib.round_to_dtype(near, W.DT_BF16)
+    for v, g in zip(near, got):
+        assert int(g) == _bf16_rne_exact(float(v)), v
 
 
 def test_double_to_f16_is_ieee_rne(oracle_lib):

@@ -99,6 +99,37 @@ def y_rel_err(y_bits: np.ndarray, y_ref: np.ndarray, dtype: int) -> float:
     return worst
 
 
+def check_selection(ref: dict, in_mask: np.ndarray, mask: np.ndarray, scores: np.ndarray,
+                    k_ff: int, tag: str = "") -> dict:
+    """Steps (a)-(d) of the parity bar, against the oracle's run `ref` (its
+    in_idx, score and ff_idx): input top-k bit-exact, the channel mask the
+    exact top-k of the GPU's own scores, scores to SCORE_TOL of the largest,
+    and the mask agreeing with the oracle's on MASK_AGREE of the channels with
+    every disagreement inside the MASK_BAND of the oracle's k-th score."""
+    f = mask.size
+    # (a) input top-k, bit-exact
+    assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"]), f"{tag}: input top-k"
+    # (b) channel selection is the exact top-k of the GPU's own scores
+    gpu_sel = oracle.topk(scores.astype(np.float64), k_ff)
+    assert np.array_equal(np.flatnonzero(mask), gpu_sel), f"{tag}: select on GPU scores"
+    assert int(mask.sum()) == k_ff
+    # (c) proxy scores
+    smax = ref["score"].max()
+    serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
+    assert serr <= SCORE_TOL * max(smax, 1e-30), f"{tag}: score err {serr} vs max {smax}"
+    # (d) mask agreement with the oracle's selection
+    ref_mask = np.zeros(f, np.uint8)
+    ref_mask[ref["ff_idx"]] = 1
+    diff = np.flatnonzero(ref_mask != mask)
+    agree = 1.0 - diff.size / f
+    tau = np.sort(ref["score"])[::-1][k_ff - 1]
+    band_ok = all(abs(ref["score"][j] - tau) <= MASK_BAND * tau for j in diff)
+    assert agree >= MASK_AGREE or diff.size == 0, f"{tag}: mask agreement {agree}"
+    assert band_ok, f"{tag}: mask disagreement outside the 1e-3 band"
+    return {"score_err_rel": serr / max(smax, 1e-30), "mask_agree": agree,
+            "mask_diff": int(diff.size)}
+
+
 def check_sparse(case: Case, x_bits: np.ndarray, k_in: int, k_ff: int, out: GpuOut,
                  tag: str = "") -> dict:
     cfg = case.cfg
@@ -107,30 +138,12 @@ def check_sparse(case: Case, x_bits: np.ndarray, k_in: int, k_ff: int, out: GpuO
                             k_in, k_ff, codes_g=case.codes_g, scales_g=case.scales_g,
                             codes_u=case.codes_u, scales_u=case.scales_u, group=cfg.group,
                             act=case.act)
-    # (a) input top-k, bit-exact
-    assert np.array_equal(np.flatnonzero(out.in_mask), ref["in_idx"]), f"{tag}: input top-k"
-    # (b) channel selection is the exact top-k of the GPU's own scores
-    gpu_sel = oracle.topk(out.scores.astype(np.float64), k_ff)
-    assert np.array_equal(np.flatnonzero(out.mask), gpu_sel), f"{tag}: select on GPU scores"
-    assert int(out.mask.sum()) == k_ff
-    # (c) proxy scores
-    smax = ref["score"].max()
-    serr = np.abs(out.scores.astype(np.float64) - ref["score"]).max()
-    assert serr <= SCORE_TOL * max(smax, 1e-30), f"{tag}: score err {serr} vs max {smax}"
-    # (d) mask agreement with the oracle's selection
-    ref_mask = np.zeros(cfg.d_ff, np.uint8)
-    ref_mask[ref["ff_idx"]] = 1
-    diff = np.flatnonzero(ref_mask != out.mask)
-    agree = 1.0 - diff.size / cfg.d_ff
-    tau = np.sort(ref["score"])[::-1][k_ff - 1]
-    band_ok = all(abs(ref["score"][j] - tau) <= MASK_BAND * tau for j in diff)
-    assert agree >= MASK_AGREE or diff.size == 0, f"{tag}: mask agreement {agree}"
-    assert band_ok, f"{tag}: mask disagreement outside the 1e-3 band"
+    stats = check_selection(ref, out.in_mask, out.mask, out.scores, k_ff, tag)
     # (e) y against the oracle on the GPU's mask
     gpu_ff = np.flatnonzero(out.mask).astype(np.int32)
     _, y_ref = oracle.stage2(x_bits, cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down,
                              gpu_ff, act=case.act)
     yerr = y_rel_err(out.y, y_ref, cfg.dtype)
     assert yerr <= Y_TOL, f"{tag}: y max-abs-rel {yerr}"
-    return {"score_err_rel": serr / max(smax, 1e-30), "mask_agree": agree,
-            "mask_diff": int(diff.size), "y_err": yerr}
+    stats["y_err"] = yerr
+    return stats

@@ -48,6 +48,25 @@ def test_c4_8192x28672_bf16():
     _full("c4_8192x28672_bf16", 3)
 
 
+@pytest.mark.parametrize("batch", [1, 6])
+def test_c2_per_row_int4_proxy(batch):
+    """The paper's own proxy format, symmetric INT4 with one scale per output
+    channel (group = d_model), at the Qwen3-8B FFN shape: batch 1 on the
+    dot-product Stage 1, batch 6 on the matrix-core Stage 1."""
+    cfg = W.CONFIGS["c2_4096x12288_bf16"].with_(group=4096, batch=batch,
+                                                 name=f"c2_per_row_int4_b{batch}")
+    mfma = prox.stage1_mfma_rows(cfg.d_model, prox.INT4, cfg.group, batch, cfg.k_in)
+    assert (mfma > 0) == (batch >= 5), mfma
+    log(f"[full] {cfg.name}: generating and packing")
+    case = make_case(cfg)
+    check_pack(case)
+    for n, x in enumerate(case.wl.x_vectors(2, batch)):
+        out = run_sparse(case, x, cfg.k_in, cfg.k_ff)
+        log(f"    {check_sparse(case, x, cfg.k_in, cfg.k_ff, out, tag=f'{cfg.name}/{n}')}")
+    del case
+    torch.cuda.empty_cache()
+
+
 def test_max_dff_matrix_core_stage2():
     """d_ff 65536 with 9 batch rows on the matrix-core Stage 2: 64 score keys
     per thread in its selection, 1024 channels per down group (the down
@@ -83,8 +102,10 @@ def c3_case():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("batch,sparsity", [(1, 0.0), (1, 0.5), (1, 0.7), (1, 0.9), (4, 0.7),
-                                            (4, 0.9), (5, 0.7), (8, 0.7), (16, 0.7), (16, 0.0)])
+@pytest.mark.parametrize("batch,sparsity", [(1, 0.0), (1, 0.5), (1, 0.7), (1, 0.9),
+                                            (4, 0.0), (4, 0.5), (4, 0.7), (4, 0.9),
+                                            (5, 0.7), (8, 0.7),
+                                            (16, 0.0), (16, 0.5), (16, 0.7), (16, 0.9)])
 def test_c3_batch_sparsity_sweep(c3_case, batch, sparsity):
     cfg = c3_case.cfg
     k_ff = W.frac_to_k(1.0 - sparsity, cfg.d_ff)

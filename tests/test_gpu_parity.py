@@ -52,6 +52,12 @@ SMALL = {
                                           in_frac=0.5, sigma_w=0.02),
     "bf16_i4_8192x700_b33": W.small_config(d=8192, f=700, batch=33, seed=19, in_frac=0.4,
                                            sigma_w=0.01),
+    # The paper's per-row INT4 proxy (one scale per output channel, group =
+    # d_model): batch 1 on the dot-product Stage 1, batch 6 on the matrix cores.
+    "bf16_i4_perrow_1024x1600_b1": W.small_config(d=1024, f=1600, batch=1, seed=21, group=1024,
+                                                  in_frac=0.4, sigma_w=0.02, n_outliers=8),
+    "bf16_i4_perrow_2048x1200_b6": W.small_config(d=2048, f=1200, batch=6, seed=22, group=2048,
+                                                  in_frac=0.4, sigma_w=0.02),
     # Maximum sizes: d_model 16384 (16 input rows per thread, 2 batch rows
     # per proxy launch) and d_ff 65536 (64 score rows per thread).
     "bf16_i4_16384x320_b3": W.small_config(d=16384, f=320, batch=3, seed=10, in_frac=0.3,

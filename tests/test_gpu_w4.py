@@ -17,7 +17,7 @@ import oracle
 from paper_2607_27591_amd import prox
 from paper_2607_27591_amd import workloads as W
 
-from gpu_cases import SCORE_TOL, Y_TOL, log, make_case, y_rel_err
+from gpu_cases import SCORE_TOL, Y_TOL, check_selection, log, make_case, y_rel_err
 from test_gpu_threshold import quantile_taus
 
 pytestmark = pytest.mark.gpu
@@ -78,19 +78,9 @@ def test_w4_sparse_parity(case):
     c, q, w4 = case
     cfg = c.cfg
     for v, x in enumerate(c.wl.x_vectors(2, cfg.batch)):
-        y, mask, in_mask, scores = _run_w4(c, q, x, cfg.k_in, cfg.k_ff)
-        ref = oracle.ffn_sparse_w4(x, cfg.dtype, w4, cfg.k_in, cfg.k_ff, codes_g=c.codes_g,
-                                   scales_g=c.scales_g, codes_u=c.codes_u, scales_u=c.scales_u,
-                                   group=cfg.group, act=c.act)
-        assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"]), f"v{v}: input top-k"
-        gpu_sel = oracle.topk(scores.astype(np.float64), cfg.k_ff)
-        assert np.array_equal(np.flatnonzero(mask), gpu_sel), f"v{v}: select on GPU scores"
-        serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
-        assert serr <= SCORE_TOL * ref["score"].max(), f"v{v}: score err {serr}"
-        _, y_ref = oracle.stage2_w4(x, cfg.dtype, w4, gpu_sel.astype(np.int32), c.act)
-        err = y_rel_err(y, y_ref, cfg.dtype)
-        log(f"    v{v}: y max-abs-rel {err:.2e}")
-        assert err <= Y_TOL, f"v{v}: y err {err}"
+        out = _run_w4(c, q, x, cfg.k_in, cfg.k_ff)
+        stats = _check_w4(c, w4, x, cfg.k_in, cfg.k_ff, out, f"v{v}")
+        log(f"    v{v}: {stats}")
 
 
 def test_w4_dense_parity_and_full_keep(case):
@@ -110,19 +100,21 @@ def test_w4_dense_parity_and_full_keep(case):
 
 
 def _check_w4(c, w4, x_bits, k_in, k_ff, out, tag):
+    """The selection bar of the 16-bit step (input top-k exact, the mask the
+    top-k of the GPU's scores, scores, mask agreement with the oracle's and
+    its band), then y against the oracle's W4 Stage 2 on the GPU's mask."""
     cfg = c.cfg
     y, mask, in_mask, scores = out
     ref = oracle.ffn_sparse_w4(x_bits, cfg.dtype, w4, k_in, k_ff, codes_g=c.codes_g,
                                scales_g=c.scales_g, codes_u=c.codes_u, scales_u=c.scales_u,
                                group=cfg.group, act=c.act)
-    assert np.array_equal(np.flatnonzero(in_mask), ref["in_idx"]), f"{tag}: input top-k"
-    gpu_sel = oracle.topk(scores.astype(np.float64), k_ff)
-    assert np.array_equal(np.flatnonzero(mask), gpu_sel), f"{tag}: select on GPU scores"
-    serr = np.abs(scores.astype(np.float64) - ref["score"]).max()
-    assert serr <= SCORE_TOL * max(ref["score"].max(), 1e-30), f"{tag}: score err {serr}"
-    _, y_ref = oracle.stage2_w4(x_bits, cfg.dtype, w4, gpu_sel.astype(np.int32), c.act)
+    stats = check_selection(ref, in_mask, mask, scores, k_ff, tag)
+    gpu_sel = np.flatnonzero(mask).astype(np.int32)
+    _, y_ref = oracle.stage2_w4(x_bits, cfg.dtype, w4, gpu_sel, c.act)
     err = y_rel_err(y, y_ref, cfg.dtype)
     assert err <= Y_TOL, f"{tag}: y err {err}"
+    stats["y_err"] = err
+    return stats
 
 
 def test_w4_extreme_k(case):
@@ -186,12 +178,7 @@ def test_w4_c4_full_size():
     q = prox.pack_w4(c.w, cfg.group)
     w4 = oracle.quantize_w4(c.wl.w_gate, c.wl.w_up, c.wl.w_down, cfg.dtype, cfg.group)
     x = c.wl.x_vectors(1, 1)[0]
-    y, mask, in_mask, scores = _run_w4(c, q, x, cfg.k_in, cfg.k_ff)
-    gpu_sel = oracle.topk(scores.astype(np.float64), cfg.k_ff)
-    assert np.array_equal(np.flatnonzero(mask), gpu_sel)
-    _, y_ref = oracle.stage2_w4(x, cfg.dtype, w4, gpu_sel.astype(np.int32))
-    err = y_rel_err(y, y_ref, cfg.dtype)
-    log(f"    c4 W4: y max-abs-rel {err:.2e}")
-    assert err <= Y_TOL
+    stats = _check_w4(c, w4, x, cfg.k_in, cfg.k_ff, _run_w4(c, q, x, cfg.k_in, cfg.k_ff), "c4 W4")
+    log(f"    c4 W4: {stats}")
     del c, q
     torch.cuda.empty_cache()

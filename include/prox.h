@@ -188,6 +188,34 @@ prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const vo
                             float *scores, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * prox_ffn_sparse without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The call allocates nothing and calls no
+ * allocating routine: it runs the same kernels as prox_ffn_sparse on the
+ * library's own device scratch, a file-scope array of
+ * PROX_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU, created with the library's code
+ * object and held until the process ends.
+ *   Arguments: as prox_ffn_sparse, without ws / ws_bytes.
+ *   Limit: prox_workspace_bytes(d_model, d_ff, batch) must not exceed
+ *   PROX_NOALLOC_SCRATCH_BYTES (e.g. 8192 x 28672 up to batch 2, d_model
+ *   16384 at batch 1), else PROX_ERR_WORKSPACE before any HIP call.
+ *   The first call on a device looks up that device's copy of the scratch
+ *   (hipGetSymbolAddress); a failure there returns PROX_ERR_HIP.
+ *   Every call on one GPU shares that GPU's scratch, which keeps the last
+ *   call's contents (the kernels need none of it initialised): calls that
+ *   overlap on one GPU (other streams, other host threads) race, so order
+ *   them, e.g. on one stream.
+ * Results are bitwise those of prox_ffn_sparse for the same arguments.
+ */
+#define PROX_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+prox_status prox_ffn_sparse_noalloc(const prox_weights *w, const prox_proxy *p, const void *x,
+                                    int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                                    uint8_t *in_mask, float *scores, hipStream_t stream);
+
+/* PROX_NOALLOC_SCRATCH_BYTES of the built library (host only). */
+size_t prox_noalloc_max_bytes(void);
+
+/*
  * The decode step with the paper's layer-wise thresholds in place of counts
  * (Sec. 4.1 masks, App. A.6 rule; thresholds calibrated offline, App. A.7):
  *   m_x = { i : max_b |x_{b,i}| >= tau_x }   (one set shared by the batch)

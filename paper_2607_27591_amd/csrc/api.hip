@@ -3,6 +3,7 @@
 #include <prox.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "kernels.hpp"
 
@@ -167,12 +168,13 @@ struct Rules {
     int32_t *counts;   // threshold mode: [k_in, k_ff] realised, or NULL
 };
 
-prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int batch,
-                        int k_in, int k_ff, const Rules &rules, void *y, uint8_t *mask,
-                        uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
-                        hipEvent_t *events, hipStream_t stream) {
-    if (!p || !p->blob || !x || !y || !mask || !ws) return PROX_ERR_INVALID;
-    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(p->blob, 16) || !aligned(ws, 256) ||
+// Host-side checks of a sparse call, workspace aside (no HIP call).  In
+// threshold mode k_in becomes the proxy's list capacity (d) and k_ff 0.
+prox_status sparse_check(const Model &m, const prox_proxy *p, const void *x, int batch,
+                         int &k_in, int &k_ff, const Rules &rules, void *y, uint8_t *mask,
+                         float *scores, hipEvent_t *events) {
+    if (!p || !p->blob || !x || !y || !mask) return PROX_ERR_INVALID;
+    if (!aligned(x, 16) || !aligned(y, 16) || !aligned(p->blob, 16) ||
         (scores && !aligned(scores, 4)))
         return PROX_ERR_INVALID;
     const int d = m.d, f = m.f;
@@ -186,13 +188,20 @@ prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int 
         return PROX_ERR_INVALID;
     }
     if (!proxy_shape_ok(d, p->fmt, p->group)) return PROX_ERR_UNSUPPORTED;
-    const int qbits = qbits_of(p->fmt);
-    if (p->bytes < BlobLayout(d, f, qbits, p->group).total) return PROX_ERR_WORKSPACE;
-    if (ws_bytes < WsLayout(d, f, batch).total) return PROX_ERR_WORKSPACE;
+    if (p->bytes < BlobLayout(d, f, qbits_of(p->fmt), p->group).total) return PROX_ERR_WORKSPACE;
     if (events)
         for (int i = 0; i <= PROX_SPARSE_STAGES; ++i)
             if (!events[i]) return PROX_ERR_INVALID;
+    return PROX_OK;
+}
 
+// The launch sequence of a checked sparse call on a workspace of at least
+// WsLayout(d, f, batch).total bytes.
+prox_status sparse_run(const Model &m, const prox_proxy *p, const void *x, int batch, int k_in,
+                       int k_ff, const Rules &rules, void *y, uint8_t *mask, uint8_t *in_mask,
+                       float *scores, void *ws, hipEvent_t *events, hipStream_t stream) {
+    const int d = m.d, f = m.f;
+    const int qbits = qbits_of(p->fmt);
     const Ws W = carve(ws, d, f, batch);
     const int dt = m.dtype;
     if (events) PROX_TRY(hipEventRecord(events[0], stream));
@@ -223,6 +232,18 @@ prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int 
                              stream);
 }
 
+prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int batch,
+                        int k_in, int k_ff, const Rules &rules, void *y, uint8_t *mask,
+                        uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
+                        hipEvent_t *events, hipStream_t stream) {
+    prox_status st = sparse_check(m, p, x, batch, k_in, k_ff, rules, y, mask, scores, events);
+    if (st != PROX_OK) return st;
+    if (!ws || !aligned(ws, 256)) return PROX_ERR_INVALID;
+    if (ws_bytes < WsLayout(m.d, m.f, batch).total) return PROX_ERR_WORKSPACE;
+    return sparse_run(m, p, x, batch, k_in, k_ff, rules, y, mask, in_mask, scores, ws, events,
+                      stream);
+}
+
 prox_status dense_impl(const Model &m, const void *x, int batch, void *y, void *ws,
                        size_t ws_bytes, hipStream_t stream) {
     if (!x || !y || !ws) return PROX_ERR_INVALID;
@@ -232,6 +253,35 @@ prox_status dense_impl(const Model &m, const void *x, int batch, void *y, void *
     const Ws W = carve(ws, m.d, m.f, batch);
     return stage2_and_reduce(m, x, batch, m.f, nullptr, nullptr, nullptr, y, W,
                              Select{0, 0.0f, nullptr}, nullptr, stream);
+}
+
+}  // namespace
+
+// Device scratch of prox_ffn_sparse_noalloc, one copy per GPU the library runs
+// on, held until the process ends.  In host code `scratch` names a host-side
+// stand-in: the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[PROX_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];   // device address of `scratch` per device, or NULL
+
+// The current device's copy of `scratch` (looked up on its first use).
+prox_status scratch_of_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return PROX_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return PROX_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return PROX_ERR_HIP;
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return PROX_OK;
 }
 
 }  // namespace
@@ -318,6 +368,25 @@ prox_status prox_ffn_sparse(const prox_weights *w, const prox_proxy *p, const vo
     return sparse_impl(model_of(w), p, x, batch, k_in, k_ff, Rules{0, 0.0f, 0.0f, nullptr}, y,
                        mask, in_mask, scores, ws, ws_bytes, nullptr, stream);
 }
+
+prox_status prox_ffn_sparse_noalloc(const prox_weights *w, const prox_proxy *p, const void *x,
+                                    int batch, int k_in, int k_ff, void *y, uint8_t *mask,
+                                    uint8_t *in_mask, float *scores, hipStream_t stream) {
+    prox_status st = check_weights(w);
+    if (st != PROX_OK) return st;
+    const Model m = model_of(w);
+    const Rules rules{0, 0.0f, 0.0f, nullptr};
+    st = sparse_check(m, p, x, batch, k_in, k_ff, rules, y, mask, scores, nullptr);
+    if (st != PROX_OK) return st;
+    if (WsLayout(m.d, m.f, batch).total > PROX_NOALLOC_SCRATCH_BYTES) return PROX_ERR_WORKSPACE;
+    void *ws = nullptr;
+    st = scratch_of_current_device(&ws);
+    if (st != PROX_OK) return st;
+    return sparse_run(m, p, x, batch, k_in, k_ff, rules, y, mask, in_mask, scores, ws, nullptr,
+                      stream);
+}
+
+size_t prox_noalloc_max_bytes(void) { return PROX_NOALLOC_SCRATCH_BYTES; }
 
 prox_status prox_ffn_sparse_tau(const prox_weights *w, const prox_proxy *p, const void *x,
                                 int batch, float tau_x, float tau_s, void *y, uint8_t *mask,

@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.prox_stage2_rows.restype = I
         L.prox_ffn_dense.argtypes = [WP, P, I, P, P, S, P]
         L.prox_ffn_sparse.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P]
+        L.prox_ffn_sparse_noalloc.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P]
+        L.prox_noalloc_max_bytes.argtypes = []
+        L.prox_noalloc_max_bytes.restype = S
         L.prox_ffn_sparse_staged.argtypes = [WP, PP, P, I, I, I, P, P, P, P, P, S, P, P]
         L.prox_ffn_sparse_tau.argtypes = [WP, PP, P, I, Z, Z, P, P, P, P, P, P, S, P]
         L.prox_reservoir_add.argtypes = [P, S, P, P, S, P]
@@ -290,6 +293,37 @@ def ffn_sparse(w: Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int, *,
         arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
         _check(lib().prox_ffn_sparse_staged(*args, arr, _stream(dev)), "prox_ffn_sparse_staged")
     return y, mask
+
+
+def ffn_sparse_noalloc(w: Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int, *,
+                       y: Optional[torch.Tensor] = None, mask: Optional[torch.Tensor] = None,
+                       in_mask: Optional[torch.Tensor] = None,
+                       scores: Optional[torch.Tensor] = None):
+    """prox_ffn_sparse_noalloc: the sparse decode step on the library's own
+    device scratch (no workspace argument; the C call allocates nothing).
+    Returns (y, mask); y and mask are allocated here when not given."""
+    x = _as_batch(x, w)
+    B = x.shape[0]
+    dev = x.device
+    y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", w.dtype)
+    mask = (torch.empty(w.d_ff, dtype=torch.uint8, device=dev) if mask is None
+            else _dev_tensor(mask, "mask", torch.uint8))
+    if in_mask is not None:
+        _dev_tensor(in_mask, "in_mask", torch.uint8)
+    if scores is not None:
+        _dev_tensor(scores, "scores", torch.float32)
+    wst, pst = w.struct(), p.struct()
+    _check(lib().prox_ffn_sparse_noalloc(ctypes.byref(wst), ctypes.byref(pst), _ptr(x), B,
+                                         int(k_in), int(k_ff), _ptr(y), _ptr(mask),
+                                         _ptr(in_mask), _ptr(scores), _stream(dev)),
+           "prox_ffn_sparse_noalloc")
+    return y, mask
+
+
+def noalloc_max_bytes() -> int:
+    """Scratch bytes per GPU of prox_ffn_sparse_noalloc (the workspace of a call
+    must fit)."""
+    return int(lib().prox_noalloc_max_bytes())
 
 
 def ffn_sparse_tau(w: Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau_s: float, *,

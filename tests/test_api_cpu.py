@@ -129,6 +129,33 @@ def test_stage2_kernel_selection():
     assert rows(4000, 14336, False, 16) == 0        # d_model % 128
 
 
+def _noalloc(w=None, p=None, x=FAKE, B=1, k_in=10, k_ff=10, y=FAKE, mask=FAKE):
+    L = prox.lib()
+    w = w if w is not None else _weights()
+    p = p if p is not None else _proxy()
+    return L.prox_ffn_sparse_noalloc(ctypes.byref(w), ctypes.byref(p), x, B, k_in, k_ff, y,
+                                     mask, None, None, None)
+
+
+def test_noalloc_checks_before_any_hip_call():
+    """The entry point without a workspace validates like prox_ffn_sparse and
+    rejects a call whose workspace would not fit its scratch, all before its
+    first HIP call (the scratch lookup)."""
+    cap = prox.noalloc_max_bytes()
+    assert cap == 32 << 20
+    assert _noalloc(k_in=0) == INVALID
+    assert _noalloc(B=65) == INVALID
+    assert _noalloc(x=None) == INVALID
+    assert _noalloc(y=MISALIGNED) == INVALID
+    assert _noalloc(p=_proxy(group=96)) == UNSUPPORTED
+    assert _noalloc(p=_proxy(nbytes=100)) == WORKSPACE
+    # 8192 x 28672: batch 2 fits the scratch, batch 4 does not.
+    big = _weights(d=8192, f=28672)
+    assert prox.workspace_bytes(8192, 28672, 2) <= cap < prox.workspace_bytes(8192, 28672, 4)
+    assert _noalloc(w=big, B=4, k_in=3277, k_ff=8602) == WORKSPACE
+    assert _noalloc(w=_weights(d=16384, f=65536), B=8, k_in=100, k_ff=100) == WORKSPACE
+
+
 def test_sparse_rejects_bad_arguments():
     L = prox.lib()
     assert _sparse(k_in=0) == INVALID

@@ -1,6 +1,6 @@
 // Device helpers shared by the gfx950 kernels of libprox: wave64 reductions
-// and scans, a block-wide radix k-th-largest search, ordered compaction and
-// 16-bit float conversions.
+// and scans, matrix-core and dot-product wrappers and 16-bit float
+// conversions.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -213,60 +213,6 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *sh, int &total) 
     total = sh[NW];
     __syncthreads();
     return res;
-}
-
-// ---------------------------------------------------------------------------
-// Block-wide k-th largest key (MSB-first radix search, 8-bit digits)
-// ---------------------------------------------------------------------------
-// Keys are held in registers: thread t owns indices t + r*NT, r < ITEMS.
-// Returns v = the k-th largest key (1 <= k <= n) and `need` = how many of the
-// keys equal to v belong to the top k (the rest of the top k is > v).
-// `hist` is LDS scratch of 256 + 2 uint32.
-template <int NT, int ITEMS, int KEYBITS>
-__device__ void block_kth_largest(const uint32_t (&keys)[ITEMS], int n, int k, uint32_t *hist,
-                                  uint32_t &v_out, int &need_out) {
-    const int tid = threadIdx.x;
-    uint32_t prefix = 0, pmask = 0;
-    int kk = k;
-#pragma unroll 1
-    for (int shift = ((KEYBITS - 1) / 8) * 8; shift >= 0; shift -= 8) {
-        for (int b = tid; b < 256; b += NT) hist[b] = 0;
-        __syncthreads();
-#pragma unroll
-        for (int r = 0; r < ITEMS; ++r) {
-            const int i = tid + r * NT;
-            if (i < n && (keys[r] & pmask) == prefix)
-                atomicAdd(&hist[(keys[r] >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        if (tid < kWave) {
-            // Lane l owns bins 255-4l ... 252-4l (descending key order).
-            const int base = 255 - 4 * tid;
-            int c0 = hist[base], c1 = hist[base - 1], c2 = hist[base - 2], c3 = hist[base - 3];
-            int local = c0 + c1 + c2 + c3;
-            int incl = wave_inclusive_scan(local);
-            int excl = incl - local;
-            if (excl < kk && kk <= incl) {
-                int cum = excl, digit = base, q = 0;
-                const int c[4] = {c0, c1, c2, c3};
-                for (q = 0; q < 4; ++q) {
-                    if (cum + c[q] >= kk) break;
-                    cum += c[q];
-                }
-                digit = base - q;
-                hist[256] = (uint32_t)digit;
-                hist[257] = (uint32_t)cum;
-            }
-        }
-        __syncthreads();
-        const uint32_t digit = hist[256];
-        kk -= (int)hist[257];
-        prefix |= digit << shift;
-        pmask |= 255u << shift;
-        __syncthreads();
-    }
-    v_out = prefix;
-    need_out = kk;
 }
 
 }  // namespace prox

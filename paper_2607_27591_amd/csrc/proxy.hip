@@ -73,15 +73,17 @@ __device__ __forceinline__ void int8_pair_fma8(uint2 a, uint2 b, uint32_t xpair,
     }
 }
 
-// Dynamic LDS of the proxy kernel: the kept-row list (row ids and x values
-// per batch row), later reused for the cross-wave reduction.
+// Dynamic LDS of the proxy kernel: the input selection's histogram, then the
+// kept-row list (row ids and x values per batch row), then the cross-wave
+// reduction.
 __host__ __device__ inline int proxy_list_cap(int k_in, int ng) {
     return (k_in + ng + 1) / 2 * 2;   // kept rows + one pad per odd group, even
 }
 __host__ __device__ inline size_t proxy_lds_bytes(int k_in, int ng, int nbt, int T) {
     const size_t list = align_up((size_t)proxy_list_cap(k_in, ng) * 2 * (1 + nbt), 16);
     const size_t red = (size_t)kMaxBlockWaves * nbt * 2 * T * 4;
-    return list > red ? list : red;
+    const size_t m = list > red ? list : red;
+    return m > kSelHistU16Bytes ? m : kSelHistU16Bytes;   // the selection's histogram first
 }
 
 // Columns each lane accumulates: 16 for one batch row of INT4 codes, else 8
@@ -149,7 +151,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     const int tile = stage1_tile<2 * T * QB / 8 < 128>(blockIdx.x, gridDim.x);
     const int ng = d / group;
 
-    __shared__ TopKScratch tk;
+    __shared__ SelScratch ss;
     __shared__ TopKOrder<C> ord;
     __shared__ int gsel0[kMaxDModel / 128 + 1];  // kept rows before each group
     __shared__ int gstart[kMaxDModel / 128 + 1]; // padded list position of each group
@@ -200,11 +202,11 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
             const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
             sel |= (uint64_t)in << r;
         }
-        topk_order<kBlock, C>(sel, d, tk, ord);
+        topk_order<kBlock, C>(sel, ord);
         if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
             *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
     } else {
-        sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+        topk_select_u15<kBlock, C>(key, d, k_in, reinterpret_cast<uint32_t *>(dsm), ss, ord);
     }
 
     // ---- group bookkeeping: kept rows per group and padded list starts ----
@@ -224,20 +226,23 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     __syncthreads();
 
     // ---- kept rows to their padded list positions (x as bf16/fp16 bits) ----
+    // The 64 inputs of a (row, wave) share one quantisation group (group is a
+    // multiple of 128), so a kept input's list position is its group's padded
+    // start plus its rank: wave-uniform table entries and a lane count.
     // i / group as a 32-bit reciprocal multiply: exact for i < 2^14 and
     // group < 2^15 (the rounding error i * group / 2^32 stays below 1 / group).
     const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;
-    auto list_pos = [&](int r) {
-        const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
-        return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
-    };
+    const int swid = wave_id();
+    int pos[C];   // list position of each of this thread's inputs, -1 if not kept
 #pragma unroll
     for (int r = 0; r < C; ++r) {
         const int i = r * kBlock + tid;
-        if (i >= d) continue;
-        const bool s = (sel >> r) & 1;
-        if (tile == 0 && in_mask) in_mask[i] = s ? 1 : 0;
-        if (s) rows_sh[list_pos(r)] = (uint16_t)i;
+        const uint64_t bs = ord.sel[r][swid];
+        const int g = (int)__umulhi((uint32_t)(r * kBlock + swid * kWave), gmagic);
+        const bool s = (bs >> lane) & 1;   // inputs past d are never kept
+        pos[r] = s ? gstart[g] - gsel0[g] + ord.off[r * kMaxBlockWaves + swid] + (int)lanes_below(bs)
+                   : -1;
+        if (s) rows_sh[pos[r]] = (uint16_t)i;
     }
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -256,7 +261,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         }
 #pragma unroll
         for (int r = 0; r < C; ++r) {
-            if (r * kBlock + tid < d && ((sel >> r) & 1)) xs_sh[b * cap + list_pos(r)] = b < nb ? xv[r] : (uint16_t)0;
+            if (pos[r] >= 0) xs_sh[b * cap + pos[r]] = b < nb ? xv[r] : (uint16_t)0;
         }
     }
     for (int g = tid; g < ng; g += kBlock) {
@@ -269,6 +274,11 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         }
     }
     __syncthreads();
+    if (tile == 0 && in_mask) {   // after the last barrier: the stores overlap the stream
+#pragma unroll
+        for (int r = 0; r < C; ++r)
+            if (r * kBlock + tid < d) in_mask[r * kBlock + tid] = pos[r] >= 0 ? 1 : 0;
+    }
 
     // ---- stream the kept row pairs: lane group l owns a contiguous range ----
     // Per group the lane accumulates x_a (M + n_a) + x_b (M + n_b) and the x

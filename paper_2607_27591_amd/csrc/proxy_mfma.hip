@@ -36,8 +36,8 @@ constexpr int kMfmaBlock = 16;    // kept input rows per block (the MFMA's K)
 constexpr int kMfmaU = 4;         // blocks in flight per wave
 
 
-// Dynamic LDS: rows [cap] u16, x [NX][cap] u16, block groups [cap / 16] u16;
-// after the stream the same space holds the cross-wave partial sums
+// Dynamic LDS: first the input selection's histogram; then rows [cap] u16,
+// x [NX][cap] u16, block groups [cap / 16] u16; after the stream the same space holds the cross-wave partial sums
 // [16 waves][64 lanes][16] f32.
 __host__ __device__ inline int mfma_list_cap(int k_in, int ng) {
     return (k_in + ng * (kMfmaBlock - 1) + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
@@ -49,7 +49,8 @@ __host__ __device__ inline size_t mfma_list_bytes(int cap, int nx) {
 constexpr size_t kMfmaRedBytes = (size_t)kMaxBlockWaves * kWave * 16 * 4;   // 64 KiB
 __host__ __device__ inline size_t mfma_lds_bytes(int k_in, int ng, int nx) {
     const size_t list = mfma_list_bytes(mfma_list_cap(k_in, ng), nx);
-    return list > kMfmaRedBytes ? list : kMfmaRedBytes;
+    const size_t m = list > kMfmaRedBytes ? list : kMfmaRedBytes;
+    return m > kSelHistU16Bytes ? m : kSelHistU16Bytes;
 }
 
 template <int DT, int T, int C, int NX>
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     const int tile = stage1_tile<T == 64>(blockIdx.x, gridDim.x);   // INT4 codes
     const int ng = d / group;
 
-    __shared__ TopKScratch tk;
+    __shared__ SelScratch ss;
     __shared__ TopKOrder<C> ord;
     __shared__ int gsel0[kMaxDModel / 128 + 1];   // kept rows before each group
     __shared__ int gstart[kMaxDModel / 128 + 1];  // padded list position of each group
@@ -97,6 +98,9 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         __syncthreads();
     };
     const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;   // i / group, exact here
+    int pos[C];   // list position of each of this thread's inputs, -1 if not kept
+#pragma unroll
+    for (int r = 0; r < C; ++r) pos[r] = -1;
     if (list_mode == kListRead) {
         // Another launch of this call selected: its list (ascending kept rows,
         // count at klist[d]) gives the same groups and list positions.
@@ -148,11 +152,11 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
                 const bool in = r * kBlock + tid < d && half_to_float<DT>((uint16_t)key[r]) >= sel_rule.tau;
                 sel |= (uint64_t)in << r;
             }
-            topk_order<kBlock, C>(sel, d, tk, ord);
+            topk_order<kBlock, C>(sel, ord);
             if (tile == 0 && row0 == 0 && tid == 0 && sel_rule.count)
                 *sel_rule.count = topk_selected_before<kBlock, C>(ord, C * kBlock);
         } else {
-            sel = topk_block<kBlock, C, false>(key, d, k_in, tk, ord, [](int) { return 0u; });
+            topk_select_u15<kBlock, C>(key, d, k_in, reinterpret_cast<uint32_t *>(dsm), ss, ord);
         }
 
         // ---- groups: kept rows per group, list starts padded to whole blocks ----
@@ -161,17 +165,18 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         group_starts();
 
         // ---- kept rows and their x values to the list ----
-        auto list_pos = [&](int r) {
-            const int g = (int)__umulhi((uint32_t)(r * kBlock + tid), gmagic);
-            return gstart[g] + topk_pos<C>(ord, r) - gsel0[g];
-        };
-        int pos[C];   // list position of each of this thread's inputs, -1 if not kept
+        // The 64 inputs of a (row, wave) share one quantisation group: a kept
+        // input's position is wave-uniform table entries plus a lane count.
+        const int swid = wave_id();
     #pragma unroll
         for (int r = 0; r < C; ++r) {
             const int i = r * kBlock + tid;
-            const bool s = i < d && ((sel >> r) & 1);
-            pos[r] = s ? list_pos(r) : -1;
-            if (tile == 0 && in_mask && i < d) in_mask[i] = s ? 1 : 0;
+            const uint64_t bs = ord.sel[r][swid];
+            const int g = (int)__umulhi((uint32_t)(r * kBlock + swid * kWave), gmagic);
+            const bool s = (bs >> lane) & 1;   // inputs past d are never kept
+            pos[r] = s ? gstart[g] - gsel0[g] + ord.off[r * kMaxBlockWaves + swid] +
+                             (int)lanes_below(bs)
+                       : -1;
             if (s) rows_sh[pos[r]] = (uint16_t)i;
         }
         // Only the nb real batch rows are stored: the stream feeds zeros for the
@@ -209,6 +214,11 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         for (int kb = p0 / kMfmaBlock; kb < p1 / kMfmaBlock; ++kb) kbg_sh[kb] = (uint16_t)g;
     }
     __syncthreads();
+    if (tile == 0 && in_mask && list_mode != kListRead) {   // stores overlap the stream
+#pragma unroll
+        for (int r = 0; r < C; ++r)
+            if (r * kBlock + tid < d) in_mask[r * kBlock + tid] = pos[r] >= 0 ? 1 : 0;
+    }
 
     // ---- stream the blocks: this wave's half and share of the blocks ----
     const int nkb = gstart[ng] / kMfmaBlock;

@@ -75,8 +75,8 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
                                             uint8_t *__restrict__ mask,
                                             float *__restrict__ scores_copy, Select sel_rule,
                                             int32_t *__restrict__ klist, int klist_mode,
-                                            TopKScratch &tk, TopKOrder<C> &ord, int *list,
-                                            int &p0_out) {
+                                            uint32_t *hist, SelScratch &ss, TopKOrder<C> &ord,
+                                            int *list, int &p0_out) {
     const int tid = threadIdx.x;
     const int nwg = gridDim.x, w = blockIdx.x;
     const bool sparse = scores != nullptr;
@@ -103,11 +103,11 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
     } else if (sparse) {
         // Item r of thread t is channel r * kBlock + t (coalesced loads).
         // Scores are |s~| >= 0, so their IEEE bit patterns order like the
-        // values.  Clamped indices, masked later: all loads are in flight at once.
+        // values; channels past f get key 0.
         uint32_t key[C];
 #pragma unroll
         for (int r = 0; r < C; ++r) {
-            key[r] = __float_as_uint(scores[min(r * kBlock + tid, f - 1)]);
+            key[r] = r * kBlock + tid < f ? __float_as_uint(scores[r * kBlock + tid]) : 0u;
         }
         uint64_t sel = 0;
         if (sel_rule.tau_mode) {
@@ -115,7 +115,7 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
 #pragma unroll
             for (int r = 0; r < C; ++r)
                 sel |= (uint64_t)(r * kBlock + tid < f && __uint_as_float(key[r]) >= sel_rule.tau) << r;
-            topk_order<kBlock, C>(sel, f, tk, ord);
+            topk_order<kBlock, C>(sel, ord);
             n_ch = topk_selected_before<kBlock, C>(ord, C * kBlock);
             // Split over the workgroups a launch for this count would have
             // (the grid is sized for every channel; the rest get none), so
@@ -126,22 +126,25 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
             n = p1 - p0;
             if (w == 0 && tid == 0 && sel_rule.count) *sel_rule.count = n_ch;
         } else {
-            sel = topk_block<kBlock, C, true>(
-                key, f, k_ff, tk, ord, [scores](int i) { return __float_as_uint(scores[i]); });
+            topk_select_f32<kBlock, C>(key, f, k_ff, hist, ss, ord);
         }
         // This workgroup's slice of positions and its chunk of the mask,
-        // straight from the order tables.
-        for (int t = tid; t < n; t += kBlock) {
-            list[t] = topk_item_at<kBlock, C>(ord, p0 + t);
-            if (klist_mode == kListWrite) klist[p0 + t] = list[t];
+        // straight from the order tables: the thread of every (row, wave)
+        // entry whose kept channels meet [p0, p1) writes them in order.
+        if (tid < C * kMaxBlockWaves) {
+            int pos = ord.off[tid];
+            uint64_t m = ord.sel[tid / kMaxBlockWaves][tid % kMaxBlockWaves];
+            if (pos < p1 && pos + __popcll(m) > p0) {
+                const int j0 = (tid / kMaxBlockWaves) * kBlock + (tid % kMaxBlockWaves) * kWave;
+                for (; m; m &= m - 1, ++pos) {
+                    if (pos < p0 || pos >= p1) continue;
+                    const int j = min(j0 + __builtin_ctzll(m), f - 1);   // rows in bounds
+                    list[pos - p0] = j;
+                    if (klist_mode == kListWrite) klist[pos] = j;
+                }
+            }
         }
         if (klist_mode == kListWrite && w == 0 && tid == 0) klist[f] = n_ch;
-        const int mchunk = (f + nwg - 1) / nwg;   // mask entries written by this workgroup
-        const int m_lo = w * mchunk, m_hi = min(m_lo + mchunk, f);
-        for (int i = m_lo + tid; i < m_hi; i += kBlock) {
-            mask[i] = topk_is_selected<kBlock, C>(ord, i) ? 1 : 0;
-            if (scores_copy) scores_copy[i] = scores[i];
-        }
         (void)sel;
         __syncthreads();
     } else {
@@ -149,6 +152,24 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
     }
     p0_out = p0;
     return n;
+}
+
+// This workgroup's chunk of the channel mask (and of the score copy) from
+// the order tables of a launch that selected.  Called after the prologue's
+// last barrier, so the stores overlap the weight stream instead of holding a
+// barrier until they are acknowledged.
+template <int C>
+__device__ __forceinline__ void stage2_mask_chunk(const TopKOrder<C> &ord, const float *scores,
+                                                  int f, uint8_t *mask, float *scores_copy,
+                                                  int klist_mode) {
+    if (!scores || klist_mode == kListRead) return;
+    const int nwg = gridDim.x, w = blockIdx.x;
+    const int mchunk = (f + nwg - 1) / nwg;   // mask entries written by this workgroup
+    const int m_lo = w * mchunk, m_hi = min(m_lo + mchunk, f);
+    for (int i = m_lo + (int)threadIdx.x; i < m_hi; i += kBlock) {
+        mask[i] = topk_is_selected<kBlock, C>(ord, i) ? 1 : 0;
+        if (scores_copy) scores_copy[i] = scores[i];
+    }
 }
 
 // WQ: 16 for 16-bit weights, 4 for INT4 codes (wt.sg/su/sd: their scales).
@@ -166,14 +187,17 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const uint16_t *__restrict__ wd = static_cast<const uint16_t *>(wt.wd);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
 
-    __shared__ TopKScratch tk;
+    __shared__ SelScratch ss;
     __shared__ TopKOrder<C> ord;
     __shared__ Stage2Smem sm;
-    extern __shared__ __align__(16) float dyn[];   // x [NB][d] or down red | s [slice][NB]
+    // The channel selection's histogram, then x [NB][d] or the down reduction
+    // | s [slice][NB].
+    extern __shared__ __align__(16) float dyn[];
 
     int p0;
     const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
-                                  klist_mode, tk, ord, sm.list, p0);
+                                  klist_mode, reinterpret_cast<uint32_t *>(dyn), ss, ord,
+                                  sm.list, p0);
     (void)p0;
 
     const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
@@ -207,6 +231,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
         }
     }
     __syncthreads();
+    stage2_mask_chunk<C>(ord, scores, f, mask, scores_copy, klist_mode);
 
     // ---- gate/up: units (channel t, part q) over the 16 waves ----
     const int Q = gateup_parts(d, NB, WQ);
@@ -519,7 +544,9 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kS2mTiles = 2;   // channel tiles per pass through the gate/up loop
 constexpr int kS2mRed = kS2mTiles * 2 * kMaxBlockWaves * kWave;   // float4 per pass
 
-size_t stage2_mfma_lds_bytes() { return (size_t)kS2mRed * 16; }
+size_t stage2_mfma_lds_bytes() {
+    return (size_t)kS2mRed * 16 > kSelHistF32Bytes ? (size_t)kS2mRed * 16 : kSelHistF32Bytes;
+}
 
 bool stage2_mfma_ok(int d, int wq) { return wq == 16 && d >= 4 * kBlock; }
 
@@ -534,16 +561,19 @@ __global__ __launch_bounds__(kBlock) void stage2_mfma_kernel(
     const uint16_t *__restrict__ wu = static_cast<const uint16_t *>(wt.wu);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
 
-    __shared__ TopKScratch tk;
+    __shared__ SelScratch ss;
     __shared__ TopKOrder<C> ord;
     __shared__ int list[kMaxSlice];
-    extern __shared__ __align__(16) float dyn[];   // red [tiles][2][waves][lanes] float4
+    // The channel selection's histogram, then red [tiles][2][waves][lanes] float4.
+    extern __shared__ __align__(16) float dyn[];
     float4 *red = reinterpret_cast<float4 *>(dyn);
 
     int p0;
     const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
-                                  klist_mode, tk, ord, list, p0);
+                                  klist_mode, reinterpret_cast<uint32_t *>(dyn), ss, ord, list,
+                                  p0);
     __syncthreads();
+    stage2_mask_chunk<C>(ord, scores, f, mask, scores_copy, klist_mode);
 
     // ---- gate/up ----
     const int nsteps = d / 32;   // steps of 32 inputs
@@ -783,8 +813,10 @@ __global__ __launch_bounds__(1024) void add_rmsnorm_kernel(const uint16_t *__res
 // Launchers
 // ---------------------------------------------------------------------------
 
-size_t stage2_lds_bytes(int d, int nbt, int wq) {
-    return align_up(stage2_head_bytes(d, nbt, wq), 16) + (size_t)kMaxSlice * nbt * 4;
+// sparse: the channel selection's histogram shares the front of the space.
+size_t stage2_lds_bytes(int d, int nbt, int wq, bool sparse) {
+    const size_t b = align_up(stage2_head_bytes(d, nbt, wq), 16) + (size_t)kMaxSlice * nbt * 4;
+    return sparse && b < kSelHistF32Bytes ? kSelHistF32Bytes : b;
 }
 
 int stage2_rows(int d, int wq) {
@@ -808,7 +840,7 @@ static hipError_t launch_stage2_t(const void *x, int nb, int d, int f, const Sta
                                   float *ypart, int ystride, int nwg, Select sel_rule, int act,
                                   int32_t *klist, int klist_mode, hipStream_t st) {
     if (WQ == 4 && !x_in_lds(d, NB)) return hipErrorInvalidValue;
-    const size_t lds = stage2_lds_bytes(d, NB, WQ);
+    const size_t lds = stage2_lds_bytes(d, NB, WQ, scores != nullptr);
     hipError_t e = allow_lds(stage2_kernel<NB, DT, C, WQ>, lds);
     if (e != hipSuccess) return e;
     stage2_kernel<NB, DT, C, WQ><<<nwg, kBlock, lds, st>>>(

@@ -2,43 +2,30 @@
 // kernels (App. A.6 per-token top-k rule, ties to the lower index).
 //
 // Items are owned strided: item r of thread t is index r * NT + t, so every
-// key load is coalesced.  Keys are unsigned 32-bit and order like the values
-// they stand for (magnitude patterns, non-negative IEEE floats).
+// key load is coalesced, and a wave's ballot over item r covers 64
+// consecutive indices.  Keys are unsigned and order like the values they
+// stand for: 15-bit magnitude patterns of 16-bit floats (input selection) or
+// bit patterns of non-negative fp32 scores (channel selection).  Items past
+// n hold key 0.
 //
-// Fast path.  Every key is shifted left by a fixed amount so that its top 16
-// significant bits (for non-negative floats: exponent and 8 mantissa bits)
-// form its "window", kept in registers, two per VGPR.  Two MSB-first radix
-// passes with 8-bit digits find the window value w* holding the k-th largest
-// key.  When all items with window w* are needed the selection is
-// {window >= w*}; otherwise, if at most one wave's worth of items share w*,
-// one wave ranks them by (full key descending, index ascending).  Any other
-// case (many equal windows) falls back to the general search below, which
-// resolves the full key and ties by index over ballots of the whole block.
+// The k-th largest key is found with histograms in LDS: one pass over all
+// 2^15 values of a 16-bit magnitude (two 16-bit counters per word), or, for
+// fp32 scores, passes over bits 30..17 of every key, then bits 16..6 and 5..0
+// of the keys that match the digits found so far, ending as soon as the found
+// bin is wholly in the top k.  A pass is one round of LDS atomics and a
+// block-wide scan of the bin counts from the top.  Ties at the k-th key are
+// cut by index: of the keys equal to it, those up to the index of the needed
+// one are in.  The selection then costs one or two compares per item: each
+// wave keeps the ballots of its rows (TopKOrder), and one scan of their
+// popcounts gives every selected item its ascending position.
 //
-// Each pass: atomics into an LDS histogram replicated kHistCopies times
-// (lane l counts into copy l % kHistCopies; score-like keys crowd a few
-// digits, and the copies turn 64-way same-address atomics into 4-way ones),
-// one barrier, all threads fold the copies (clearing them for the next pass),
-// one barrier, and every wave scans the 256 digit counts itself, so no
-// broadcast barrier is needed.
+// Per-item work is what these prologues cost: a 1024-thread block runs 16
+// waves on 4 SIMDs, so every instruction per item is ~16 CU cycles per row.
 #pragma once
 
 #include "common.hpp"
 
 namespace prox {
-
-constexpr int kHistCopies = 16;
-
-struct alignas(16) TopKScratch {
-    uint32_t hist[256 * kHistCopies];   // [digit][copy]; later selection words
-    uint32_t cnt[256];                  // folded digit counts
-    uint32_t pick[2];
-    uint32_t wmax[kMaxBlockWaves];
-    int scan[kMaxBlockWaves + 1];
-    uint32_t cand_key[kWave];           // final-bucket candidates (fast path)
-    int cand_idx[kWave];
-    int cand_n;
-};
 
 // Per (item row r, wave w) ballots of the selected items and their exclusive
 // prefix counts in index order.
@@ -48,361 +35,423 @@ struct TopKOrder {
     int off[C * kMaxBlockWaves];
 };
 
-template <int NT>
-__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, TopKScratch &sh) {
-    constexpr int NW = NT / kWave;
-    v = wave_max_u32(v);
-    if (lane_id() == 0) sh.wmax[threadIdx.x / kWave] = v;
-    __syncthreads();
-    uint32_t m = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) m = max(m, sh.wmax[w]);
-    __syncthreads();
-    return m;
+// Scratch of the digit search (besides the histogram).
+struct SelScratch {
+    int wtot[kMaxBlockWaves];   // per-wave totals of the bin scan
+    int pick[3];                // found digit, rank inside it, its count
+};
+
+// The 2^14-word histograms are padded by one word after every 16, so the 16
+// words a thread scans start 17 words after its neighbour's: the scan's LDS
+// reads are free of bank conflicts.  Word w sits at hist_pad(w).
+__host__ __device__ constexpr uint32_t hist_pad(uint32_t w) { return w + (w >> 4); }
+constexpr int kSelPadWords = 16384 + 1024;
+
+// LDS words of the histograms: 2^15 packed 16-bit counters (input keys), or
+// 2^14 + 2^11 + 2^6 counters (the three digits of a score key).
+constexpr int kSelHistU16Words = kSelPadWords;
+constexpr int kSelHistF32Words = kSelPadWords + 2048 + 64;
+constexpr size_t kSelHistU16Bytes = (size_t)kSelHistU16Words * 4;
+constexpr size_t kSelHistF32Bytes = (size_t)kSelHistF32Words * 4;
+
+// Wave index as a wave-uniform value (kept in an SGPR).
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
 }
 
-// ---- general search (fallback) ----
-// Keys through an accessor K:
-//   K::hi(r)        the key of item r with its low 16 bits cleared, for a
-//                   compile-time r (held in registers),
-//   K::kHasLow      whether keys have low bits at all,
-//   K::full_dyn(r)  the complete key for a run-time r (reads memory).
-// Full keys are only read for items whose high half ties with the threshold
-// prefix, visited by a bit loop.
-//
-// v = the k-th largest of the n keys (1 <= k <= n); need = how many of the
-// keys equal to v belong to the top k (every key > v does).
-template <int NT, int C, typename K>
-__device__ __forceinline__ void topk_threshold(const K &keys, int n, int k, TopKScratch &sh, uint32_t &v_out,
-                               int &need_out) {
-    const int tid = threadIdx.x, lane = lane_id();
-    uint32_t kmax = 0;
+// Lanes 0 .. m - 1 of a wave (all for m >= 64, none for m <= 0).
+__device__ __forceinline__ uint64_t lanes_first(int m) {
+    return m >= kWave ? ~0ull : m <= 0 ? 0ull : ((1ull << m) - 1);
+}
+
+// Lanes of wave wid whose item r * NT + tid is below n (wave-uniform).
+template <int NT>
+__device__ __forceinline__ uint64_t lanes_valid(int r, int wid, int n) {
+    return lanes_first(n - (r * NT + wid * kWave));
+}
+
+// v_writelane (lane `lane` of v replaced by the wave-uniform s) through its
+// LLVM intrinsic, so the compiler also inserts the wait states it needs
+// after the instruction that wrote s.
+extern "C" __device__ int prox_llvm_writelane(int s, int lane, int v) __asm("llvm.amdgcn.writelane.i32");
+
+__device__ __forceinline__ uint32_t write_lane(uint32_t v, uint32_t s, int lane) {
+    return (uint32_t)prox_llvm_writelane((int)s, lane, (int)v);
+}
+
+// Every wave's row ballots to ord.sel: lane r of two registers takes row r's
+// ballot (lanes r < C), then one store per wave.
+template <int C, typename B>
+__device__ __forceinline__ void store_ballots(TopKOrder<C> &ord, int wid, B &&ballot_of_row) {
+    uint32_t lo = 0, hi = 0;
 #pragma unroll
     for (int r = 0; r < C; ++r) {
-            if (r * NT + tid < n) kmax = max(kmax, keys.hi(r));
+        const uint64_t b = ballot_of_row(r);
+        lo = write_lane(lo, (uint32_t)b, r);
+        hi = write_lane(hi, (uint32_t)(b >> 32), r);
     }
-    kmax = block_max_u32<NT>(kmax, sh);
-    // With every high half zero only the low half (if any) is searched.
-    const int top_shift = kmax ? ((31 - __clz(kmax)) / 8) * 8 : (K::kHasLow ? 8 : 16);
-    uint32_t prefix = 0, pmask = 0;
-    int kk = k;
-    const int copy = lane % kHistCopies;
-    uint64_t cand = 0;   // items whose high half matches the prefix (low-half passes)
-    const int last_shift = K::kHasLow ? 0 : 16;
-#pragma unroll 1
-    for (int shift = top_shift; shift >= last_shift; shift -= 8) {
-        for (int b = tid; b < 256 * kHistCopies / 4; b += NT)
-            reinterpret_cast<uint4 *>(sh.hist)[b] = make_uint4(0, 0, 0, 0);
-        __syncthreads();
-        if (shift >= 16) {
-#pragma unroll
-            for (int r = 0; r < C; ++r) {
-                if (r * NT + tid >= n) continue;
-                const uint32_t kh = keys.hi(r);
-                if ((kh & pmask) == prefix)
-                    atomicAdd(&sh.hist[((kh >> shift) & 255u) * kHistCopies + copy], 1u);
-            }
-        } else {
-            if (shift == 8) {   // the high half is settled: collect its ties once
-#pragma unroll
-                for (int r = 0; r < C; ++r) {
-                        if (r * NT + tid < n && keys.hi(r) == (prefix & 0xFFFF0000u)) cand |= 1ull << r;
-                }
-            }
-            for (uint64_t m = cand; m; m &= m - 1) {
-                const uint32_t key = keys.full_dyn(__builtin_ctzll(m));
-                if ((key & pmask) == prefix)
-                    atomicAdd(&sh.hist[((key >> shift) & 255u) * kHistCopies + copy], 1u);
-            }
-        }
-        __syncthreads();
-        if (tid < kWave) {
-            // Lane l owns digits 255-4l ... 252-4l, i.e. descending key order.
-            const int base = 255 - 4 * tid;
-            int cnt[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const uint4 *h = reinterpret_cast<const uint4 *>(&sh.hist[(base - q) * kHistCopies]);
-                int s = 0;
-#pragma unroll
-                for (int z = 0; z < kHistCopies / 4; ++z) {
-                    const uint4 v4 = h[z];
-                    s += (int)(v4.x + v4.y + v4.z + v4.w);
-                }
-                cnt[q] = s;
-            }
-            const int local = cnt[0] + cnt[1] + cnt[2] + cnt[3];
-            const int incl = wave_inclusive_scan(local);
-            const int excl = incl - local;
-            if (excl < kk && kk <= incl) {
-                int cum = excl, q = 0;
-                for (q = 0; q < 3; ++q) {
-                    if (cum + cnt[q] >= kk) break;
-                    cum += cnt[q];
-                }
-                sh.pick[0] = (uint32_t)(base - q);
-                sh.pick[1] = (uint32_t)cum;
-            }
-        }
-        __syncthreads();
-        const uint32_t digit = sh.pick[0];
-        kk -= (int)sh.pick[1];
-        prefix |= digit << shift;
-        pmask |= 255u << shift;
-        __syncthreads();
-    }
-    v_out = prefix;
-    need_out = kk;
+    const int lane = lane_id();
+    if (lane < C) ord.sel[lane][wid] = ((uint64_t)hi << 32) | lo;
 }
 
-// Exclusive scan, in (r, w) order, of the C * 16 per-wave counts in off[]
-// (written before the call by lane 0 of each wave).  One wave does it: lane l
-// holds C / 4 consecutive entries.
+// Exclusive scan of the per-(row, wave) counts, taken as the popcounts of the
+// ballots in ord.sel (written before the call), into ord.off.  One wave does
+// it: lane l holds C / 4 consecutive entries.
 template <int NT, int C>
-__device__ __forceinline__ void topk_scan_table(int *off, TopKScratch &) {
+__device__ __forceinline__ void topk_scan_ballots(TopKOrder<C> &ord) {
     static_assert(C % 4 == 0 && C * kMaxBlockWaves == kWave * (C / 4), "C / 4 entries per lane");
     constexpr int E = C / 4;
     __syncthreads();
     if (threadIdx.x < kWave) {
         const int lane = lane_id();
+        const uint64_t *sel = &ord.sel[0][0];
         int v[E], run = 0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             v[e] = run;
-            run += off[lane * E + e];
+            run += __popcll(sel[lane * E + e]);
         }
         const int base = wave_inclusive_scan(run) - run;
 #pragma unroll
-        for (int e = 0; e < E; ++e) off[lane * E + e] = base + v[e];
+        for (int e = 0; e < E; ++e) ord.off[lane * E + e] = base + v[e];
     }
     __syncthreads();
 }
 
-// Selection bits of the top k given v and need from topk_threshold (bit r =
-// item r); ord.off serves as scratch for ranking the keys equal to v.
-template <int NT, int C, typename K>
-__device__ __forceinline__ uint64_t topk_select_general(const K &keys, int n, uint32_t v, int need,
-                                                        TopKScratch &sh, TopKOrder<C> &ord) {
-    static_assert(C <= 64, "selection bits fit in 64");
-    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
-    uint64_t gt = 0, eq = 0;
-    const uint32_t vh = v & 0xFFFF0000u;
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-        if (r * NT + tid >= n) continue;
-        const uint32_t kh = keys.hi(r);
-        gt |= (uint64_t)(kh > vh) << r;
-        eq |= (uint64_t)(kh == vh) << r;
-    }
-    if (K::kHasLow) {   // settle high-half ties on the full key
-        for (uint64_t m = eq; m; m &= m - 1) {
-            const int r = __builtin_ctzll(m);
-            const uint32_t kf = keys.full_dyn(r);
-            if (kf > v) gt |= 1ull << r;
-            if (kf != v) eq &= ~(1ull << r);
-        }
-    }
-    // Rank the keys equal to v in index order; the first `need` are kept.
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-        const uint64_t m = __ballot((eq >> r) & 1);
-        if (lane == 0) ord.off[r * kMaxBlockWaves + wid] = __popcll(m);
-    }
-    topk_scan_table<NT, C>(ord.off, sh);
-    uint64_t sel = gt;
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-        const uint64_t m = __ballot((eq >> r) & 1);
-        if ((eq >> r) & 1) {
-            const int rank = ord.off[r * kMaxBlockWaves + wid] + (int)lanes_below(m);
-            if (rank < need) sel |= 1ull << r;
-        }
-    }
-    __syncthreads();   // ord.off is rewritten by topk_order
-    return sel;
-}
-
-// Ascending positions of the selected items: per (row, wave) ballots and their
-// exclusive prefix counts in index order.
+// Ascending positions of the selected items (bit r of sel = item r): per
+// (row, wave) ballots and their exclusive prefix counts in index order.
 template <int NT, int C>
-__device__ __forceinline__ void topk_order(uint64_t sel, int n, TopKScratch &sh, TopKOrder<C> &ord) {
-    static_assert(C <= kWave, "one row per lane");
-    const int wid = threadIdx.x / kWave, lane = lane_id();
-    uint64_t mine = 0;   // lane r keeps row r's ballot (rows past n stay empty)
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-        const uint64_t m = __ballot((sel >> r) & 1);
-        mine = lane == r ? m : mine;
-    }
-    if (lane < C) {
-        ord.sel[lane][wid] = mine;
-        ord.off[lane * kMaxBlockWaves + wid] = __popcll(mine);
-    }
-    topk_scan_table<NT, C>(ord.off, sh);
+__device__ __forceinline__ void topk_order(uint64_t sel, TopKOrder<C> &ord) {
+    store_ballots<C>(ord, wave_id(), [&](int r) { return __ballot((sel >> r) & 1); });
+    topk_scan_ballots<NT, C>(ord);
 }
 
-// ---- fast path ----
-// One radix pass over the items for which item(r, digit) is true: returns the
-// digit holding the kk-th largest (counting from the top), kk's rank inside
-// that digit, and the digit's item count.  sh.hist must be zero on entry and
-// is zero again on return.
-template <int NT, int C, typename Item>
-__device__ __forceinline__ void topk_pass(const Item &item, int n, TopKScratch &sh, int &kk,
-                                          uint32_t &digit, int &bucket) {
-    static_assert(NT == 256 * kHistCopies / 4, "one uint4 of copies per thread");
-    const int tid = threadIdx.x, lane = lane_id();
-    const int copy = lane % kHistCopies;
+// The bin holding the kk-th largest counted item (1 <= kk <= total count).
+// The NBINS counters are in ascending digit order; PACKED holds two 16-bit
+// counters per word, bin 2i in the low half of word i.  Thread t owns the BPT
+// bins just below NBINS - t * BPT, so the threads in order walk the digits
+// downwards and one block-wide scan of their sums finds the bin.  Returns, in
+// every thread, the digit, kk's rank inside that bin and the bin's count.
+template <int NBINS, bool PACKED>
+__device__ __forceinline__ void find_digit(const uint32_t *h, int kk, SelScratch &ss,
+                                           uint32_t &digit, int &kk_in, int &bucket) {
+    constexpr int BPT = NBINS >= kBlock ? NBINS / kBlock : 1;   // bins per thread
+    constexpr int PER = PACKED ? 2 : 1;                         // bins per word
+    constexpr int WPT = BPT / PER;                              // words per thread
+    static_assert(NBINS % kBlock == 0 || NBINS <= kBlock, "bins split evenly");
+    static_assert(BPT % PER == 0 && (WPT == 1 || WPT == 2 || WPT % 4 == 0), "whole words");
+    const int tid = threadIdx.x, lane = lane_id(), wid = wave_id();
+    const bool own = tid * BPT < NBINS;
+    const int lo_bin = NBINS - (tid + 1) * BPT;   // lowest bin of this thread
+    uint32_t w[WPT];
+    if (own) {
+        const uint32_t *src = h + lo_bin / PER;
+        if constexpr (WPT == 16) {
+            // A 2^14-word histogram, padded (hist_pad): 17 words per thread.
+            const uint32_t *p = h + hist_pad((uint32_t)(lo_bin / PER));
 #pragma unroll
-    for (int r = 0; r < C; ++r) {
-        uint32_t dg;
-        if (item(r, dg)) atomicAdd(&sh.hist[dg * kHistCopies + copy], 1u);
-    }
-    __syncthreads();
-    {
-        const int dgt = tid / 4;
-        uint4 *h = reinterpret_cast<uint4 *>(&sh.hist[dgt * kHistCopies]) + (tid % 4);
-        const uint4 c4 = *h;
-        *h = make_uint4(0, 0, 0, 0);
-        uint32_t t = c4.x + c4.y + c4.z + c4.w;
-        t = quad_sum_u32(t);
-        if ((tid % 4) == 0) sh.cnt[dgt] = t;
-    }
-    __syncthreads();
-    // Lane l holds digits 255-4l ... 252-4l (descending key order).
-    const uint4 c4 = *reinterpret_cast<const uint4 *>(&sh.cnt[252 - 4 * lane]);
-    const int c0 = (int)c4.w, c1 = (int)c4.z, c2 = (int)c4.y, c3 = (int)c4.x;
-    const int local = c0 + c1 + c2 + c3;
-    const int incl = wave_inclusive_scan(local);
-    const int excl = incl - local;
-    const uint64_t hit = __ballot(excl < kk && kk <= incl);
-    const int src = __builtin_ctzll(hit);   // exactly one lane: 1 <= kk <= total
-    int q, cum = excl, cq;
-    if (kk <= cum + c0) { q = 0; cq = c0; }
-    else if (kk <= cum + c0 + c1) { q = 1; cum += c0; cq = c1; }
-    else if (kk <= cum + c0 + c1 + c2) { q = 2; cum += c0 + c1; cq = c2; }
-    else { q = 3; cum += c0 + c1 + c2; cq = c3; }
-    digit = (uint32_t)__shfl(255 - 4 * lane - q, src, kWave);
-    kk -= __shfl(cum, src, kWave);
-    bucket = __shfl(cq, src, kWave);
-}
-
-// Window keys (top 16 bits of the shifted keys) for the general search.
-template <int NT, int C2, bool HL, typename Reload>
-struct WinKeys {
-    static constexpr bool kHasLow = HL;
-    const uint32_t (&h2)[C2];
-    const Reload &reload;
-    int shift;
-    __device__ uint32_t hi(int r) const {
-        const uint32_t w = h2[r >> 1];
-        return (r & 1) ? (w & 0xFFFF0000u) : (w << 16);
-    }
-    __device__ uint32_t full_dyn(int r) const { return reload(r * NT + (int)threadIdx.x) << shift; }
-};
-
-// Top k of n keys (1 <= k <= n).  key[r] is item r's key (any value when its
-// index is >= n); reload(i) returns key i again (only called when kHasLow:
-// keys with bits below their 16-bit window).  Returns the selection bits and
-// fills ord with the ascending positions of the selected items.
-template <int NT, int C, bool kHasLow, typename Reload>
-__device__ __forceinline__ uint64_t topk_block(const uint32_t (&key)[C], int n, int k, TopKScratch &sh,
-                                               TopKOrder<C> &ord, const Reload &reload) {
-    static_assert(C % 2 == 0 && C <= 64, "paired windows, 64 selection bits");
-    const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
-    // Fixed windows: non-negative IEEE floats (kHasLow) have bit 31 clear, so
-    // key << 1 puts the exponent and the top 8 mantissa bits in the high
-    // half; keys of at most 16 bits are the window themselves.
-    constexpr int shift = kHasLow ? 1 : 16;
-    for (int b = tid; b < 256 * kHistCopies / 4; b += NT)
-        reinterpret_cast<uint4 *>(sh.hist)[b] = make_uint4(0, 0, 0, 0);
-    __syncthreads();
-    uint32_t h2[C / 2];
-    // Low key halves, two per word, kept for the tie step where registers
-    // allow (up to 32 rows); otherwise they are reloaded.
-    constexpr bool kLowRegs = kHasLow && C <= 32;
-    uint32_t l2[kLowRegs ? C / 2 : 1];
+            for (int j = 0; j < WPT; ++j) w[j] = p[j];
+        } else if constexpr (WPT % 4 == 0) {
 #pragma unroll
-    for (int q = 0; q < C / 2; ++q) {   // rows past n hold junk and are never read
-        h2[q] = ((key[2 * q] << shift) >> 16) | ((key[2 * q + 1] << shift) & 0xFFFF0000u);
-        if constexpr (kLowRegs) l2[q] = (key[2 * q] & 0xFFFFu) | (key[2 * q + 1] << 16);
-    }
-    auto win = [&](int r) -> uint32_t { return (r & 1) ? (h2[r >> 1] >> 16) : (h2[r >> 1] & 0xFFFFu); };
-    auto valid = [&](int r) { return r * NT + tid < n; };
-
-    int kk = k, bucket;
-    uint32_t da, db;
-    topk_pass<NT, C>([&](int r, uint32_t &dg) { dg = win(r) >> 8; return valid(r); }, n, sh, kk, da, bucket);
-    uint64_t sel = 0;
-    if (kk == bucket) {   // every item with this top digit is in
-#pragma unroll
-        for (int r = 0; r < C; ++r) {
-            sel |= (uint64_t)(valid(r) && (win(r) >> 8) >= da) << r;
+            for (int j = 0; j < WPT / 4; ++j) {
+                const uint4 v = reinterpret_cast<const uint4 *>(src)[j];
+                w[4 * j] = v.x; w[4 * j + 1] = v.y; w[4 * j + 2] = v.z; w[4 * j + 3] = v.w;
+            }
+        } else if constexpr (WPT == 2) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(src);
+            w[0] = v.x; w[1] = v.y;
+        } else {
+            w[0] = src[0];
         }
     } else {
-        if (tid == 0) sh.cand_n = 0;   // not touched again before the next barrier
-        topk_pass<NT, C>([&](int r, uint32_t &dg) { dg = win(r) & 255u; return valid(r) && (win(r) >> 8) == da; },
-                         n, sh, kk, db, bucket);
-        const uint32_t w_star = (da << 8) | db;
 #pragma unroll
-        for (int r = 0; r < C; ++r) {
-            sel |= (uint64_t)(valid(r) && win(r) > w_star) << r;
+        for (int j = 0; j < WPT; ++j) w[j] = 0;
+    }
+    // Packed words are summed whole (each half stays below 2^16), then the
+    // two halves added.
+    int local;
+    if constexpr (PACKED) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int j = 0; j < WPT; ++j) t += w[j];
+        local = (int)((t & 0xFFFFu) + (t >> 16));
+    } else {
+        local = 0;
+#pragma unroll
+        for (int j = 0; j < WPT; ++j) local += (int)w[j];
+    }
+    const int incl = wave_inclusive_scan(local);
+    if (lane == kWave - 1) ss.wtot[wid] = incl;
+    __syncthreads();
+    // Counts of the waves before this one: lanes 0..15 scan the 16 totals.
+    int base = 0;
+    if (wid > 0) {
+        int t = lane < kMaxBlockWaves ? ss.wtot[lane] : 0;
+        t += __builtin_amdgcn_update_dpp(0, t, 0x111, 0xF, 0xF, false);   // row_shr:1
+        t += __builtin_amdgcn_update_dpp(0, t, 0x112, 0xF, 0xF, false);   // row_shr:2
+        t += __builtin_amdgcn_update_dpp(0, t, 0x114, 0xF, 0xF, false);   // row_shr:4
+        t += __builtin_amdgcn_update_dpp(0, t, 0x118, 0xF, 0xF, false);   // row_shr:8
+        base = __builtin_amdgcn_readlane(t, wid - 1);
+    }
+    const int excl = base + incl - local;
+    if (own && excl < kk && kk <= excl + local) {   // exactly one thread
+        // Words from the top down: the first whose running count reaches kk.
+        int cum = excl, jw = 0;
+        uint32_t ww = 0;
+        bool found = false;
+#pragma unroll
+        for (int j = WPT - 1; j >= 0; --j) {
+            const int c = PACKED ? (int)((w[j] & 0xFFFFu) + (w[j] >> 16)) : (int)w[j];
+            if (!found && cum + c >= kk) {
+                found = true;
+                jw = j;
+                ww = w[j];
+            } else if (!found) {
+                cum += c;
+            }
         }
-        if (kk == bucket) {
-#pragma unroll
-            for (int r = 0; r < C; ++r) {
-                sel |= (uint64_t)(valid(r) && win(r) == w_star) << r;
+        int bin, cnt;
+        if constexpr (PACKED) {
+            const int hi = (int)(ww >> 16);
+            if (cum + hi >= kk) {
+                bin = lo_bin + 2 * jw + 1;
+                cnt = hi;
+            } else {
+                cum += hi;
+                bin = lo_bin + 2 * jw;
+                cnt = (int)(ww & 0xFFFFu);
             }
-        } else if (bucket <= kWave) {
-            // Gather the bucket (slot order is arbitrary; ranking is explicit).
-            // The histogram is idle now: its first NT 64-bit words become
-            // per-thread selection words for the bucket items.
-            uint64_t *selw = reinterpret_cast<uint64_t *>(sh.hist);
-            static_assert(sizeof(sh.hist) >= NT * sizeof(uint64_t), "selection words fit");
-            selw[tid] = 0;
-#pragma unroll
-            for (int r = 0; r < C; ++r) {
-                if (valid(r) && win(r) == w_star) {
-                    const int i = r * NT + tid;
-                    const int slot = atomicAdd(&sh.cand_n, 1);
-                    uint32_t ck = w_star << 16;
-                    if constexpr (kLowRegs) {
-                        const uint32_t lo = (r & 1) ? (l2[r >> 1] >> 16) : (l2[r >> 1] & 0xFFFFu);
-                        ck |= (lo << shift) & 0xFFFFu;   // the shifted key's low half
-                    } else if constexpr (kHasLow) {
-                        ck = reload(i) << shift;
-                    }
-                    sh.cand_key[slot] = ck;
-                    sh.cand_idx[slot] = i;
-                }
-            }
-            __syncthreads();
-            if (wid == 0) {
-                // Lane l holds candidate l; the others are read with readlane.
-                const bool act = lane < bucket;
-                const uint32_t mk = act ? sh.cand_key[lane] : 0u;
-                const int mi = act ? sh.cand_idx[lane] : 0;
-                int rank = 0;
-                for (int j = 0; j < bucket; ++j) {
-                    const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mk, j);
-                    const int ij = __builtin_amdgcn_readlane(mi, j);
-                    rank += (kj > mk || (kj == mk && ij < mi)) ? 1 : 0;
-                }
-                if (act && rank < kk)
-                    atomicOr(reinterpret_cast<unsigned long long *>(&selw[mi % NT]), 1ull << (mi / NT));
-            }
-            __syncthreads();
-            sel |= selw[tid];
         } else {
-            // Many items share the window: general search on the shifted keys.
-            const WinKeys<NT, C / 2, kHasLow, Reload> wk{h2, reload, shift};
-            uint32_t v;
-            int need;
-            topk_threshold<NT, C>(wk, n, k, sh, v, need);
-            sel = topk_select_general<NT, C>(wk, n, v, need, sh, ord);
+            bin = lo_bin + jw;
+            cnt = (int)ww;
+        }
+        ss.pick[0] = bin;
+        ss.pick[1] = kk - cum;
+        ss.pick[2] = cnt;
+    }
+    __syncthreads();
+    digit = (uint32_t)ss.pick[0];
+    kk_in = ss.pick[1];
+    bucket = ss.pick[2];
+}
+
+// The top-k rule once the threshold is known: every key above v is in; of the
+// keys equal to v, those with index <= istar (istar >= n: all of them).
+struct SelRule {
+    uint32_t v;
+    int istar;
+};
+
+// Order tables of `rule`: the ballot of every (row, wave) and, after one scan
+// of their popcounts, the exclusive prefix counts of the selected items in
+// index order.  Per item one compare, two for a tie cut.
+template <int NT, int C>
+__device__ __forceinline__ void topk_table(const uint32_t (&key)[C], int n, SelRule rule,
+                                           TopKOrder<C> &ord) {
+    const int wid = wave_id();
+    // Items past n hold key 0, so only a rule that admits 0 needs their lanes
+    // masked.
+    const bool mask = rule.v == 0;
+    if (rule.istar >= n) {
+        store_ballots<C>(ord, wid, [&](int r) {
+            const uint64_t b = __ballot(key[r] >= rule.v);
+            return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+        });
+    } else {
+        store_ballots<C>(ord, wid, [&](int r) {
+            const int base = r * NT + wid * kWave;   // index of lane 0 of this wave
+            const uint64_t b = __ballot(key[r] > rule.v) |
+                               (__ballot(key[r] == rule.v) & lanes_first(rule.istar - base + 1));
+            return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+        });
+    }
+    topk_scan_ballots<NT, C>(ord);
+}
+
+// Index of the need-th (from 1) key equal to v in index order; uses ord as
+// scratch (the caller rebuilds it afterwards).
+template <int NT, int C>
+__device__ __forceinline__ int topk_tie_index(const uint32_t (&key)[C], int n, uint32_t v,
+                                              int need, TopKOrder<C> &ord, SelScratch &ss) {
+    const int wid = wave_id();
+    const bool mask = v == 0;   // items past n hold key 0
+    store_ballots<C>(ord, wid, [&](int r) {
+        const uint64_t b = __ballot(key[r] == v);
+        return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+    });
+    topk_scan_ballots<NT, C>(ord);
+    // The entry holding the need-th equal key (one thread finds it), then the
+    // set bit inside that entry's ballot.
+    const int e = threadIdx.x;
+    if (e < C * kMaxBlockWaves) {
+        const int before = ord.off[e];
+        uint64_t m = ord.sel[e / kMaxBlockWaves][e % kMaxBlockWaves];
+        if (before < need && need <= before + __popcll(m)) {
+            int q = need - 1 - before;   // the q-th set bit (from 0) of m
+            int bit = 0;
+#pragma unroll
+            for (int half = 32; half >= 1; half >>= 1) {
+                const int c = __popcll(m & ((1ull << half) - 1));
+                if (q >= c) { q -= c; m >>= half; bit += half; }
+                else m &= (1ull << half) - 1;
+            }
+            ss.pick[0] = (e / kMaxBlockWaves) * NT + (e % kMaxBlockWaves) * kWave + bit;
         }
     }
-    topk_order<NT, C>(sel, n, sh, ord);
-    return sel;
+    __syncthreads();
+    const int istar = ss.pick[0];
+    __syncthreads();   // every thread has read ss.pick and ord
+    return istar;
+}
+
+// One narrow digit pass: counts bits [shift, shift + log2 NBINS) of the keys
+// whose higher bits equal `prefix` (bits from `shift + log2 NBINS` up), into
+// h (NBINS words, zero), then finds the bin holding the kk-th largest.
+template <int NT, int C, int NBINS>
+__device__ __forceinline__ void narrow_pass(const uint32_t (&key)[C], int n, int shift,
+                                            uint32_t prefix, uint32_t *h, SelScratch &ss,
+                                            int &kk, int &bucket, uint32_t &digit) {
+    const int lane = lane_id(), wid = wave_id();
+    constexpr uint32_t kMaskBins = NBINS - 1;
+    const int top = shift + __builtin_ctz(NBINS);   // bits at or above top: the prefix
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+        // Keys past n are 0: masked whenever the prefix admits 0.
+        const bool match = top >= 32 || (key[r] >> top) == prefix;
+        const uint64_t b = __ballot(match) & (prefix == 0 ? lanes_valid<NT>(r, wid, n) : ~0ull);
+        if ((b >> lane) & 1) atomicAdd(&h[(key[r] >> shift) & kMaskBins], 1u);
+    }
+    __syncthreads();
+    find_digit<NBINS, false>(h, kk, ss, digit, kk, bucket);
+}
+
+// Top k (1 <= k <= n) of 15-bit keys (magnitude patterns of 16-bit floats):
+// one histogram pass over all 2^15 values finds the k-th largest key v; ties
+// at v are cut by index.  hist: kSelHistU16Words words of LDS.  Fills ord.
+template <int NT, int C>
+__device__ __forceinline__ void topk_select_u15(const uint32_t (&key)[C], int n, int k,
+                                                uint32_t *hist, SelScratch &ss,
+                                                TopKOrder<C> &ord) {
+    static_assert(C * NT < 65536, "a 16-bit counter holds every key");
+    const int tid = threadIdx.x;
+    if constexpr (C * NT <= 4096) {
+        // Few keys: bits 14..7, then 6..0, over 256- and 128-bin histograms.
+        uint32_t *h1 = hist, *h2 = hist + 256;
+        for (int i = tid; i < (256 + 128) / 4; i += NT)
+            reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
+        __syncthreads();
+        int kk = k, bucket;
+        uint32_t d1, d2;
+        narrow_pass<NT, C, 256>(key, n, 7, 0, h1, ss, kk, bucket, d1);
+        SelRule rule{d1 << 7, n};
+        if (kk < bucket) {
+            narrow_pass<NT, C, 128>(key, n, 0, d1, h2, ss, kk, bucket, d2);
+            rule.v = (d1 << 7) | d2;
+            if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, rule.v, kk, ord, ss);
+        }
+        topk_table<NT, C>(key, n, rule, ord);
+        return;
+    }
+    for (int i = tid; i < kSelHistU16Words / 4; i += NT)
+        reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < C; ++r) atomicAdd(&hist[hist_pad(key[r] >> 1)], 1u << ((key[r] & 1u) << 4));
+    if (tid == 0 && n < C * NT) atomicSub(&hist[0], (uint32_t)(C * NT - n));   // the items past n
+    __syncthreads();
+    uint32_t v;
+    int need, bucket;
+    find_digit<32768, true>(hist, k, ss, v, need, bucket);
+    SelRule rule{v, n};
+    if (need < bucket) rule.istar = topk_tie_index<NT, C>(key, n, v, need, ord, ss);
+    topk_table<NT, C>(key, n, rule, ord);
+}
+
+// Top k (1 <= k <= n) of non-negative fp32 keys (bit 31 clear): bits 30..17
+// of every key, then bits 16..6 and 5..0 of the keys matching the digits
+// found so far (a wave row with none of them is skipped whole), until the
+// found bin is wholly in the top k; ties at the k-th key are cut by index.
+// hist: kSelHistF32Words words of LDS.  Fills ord.
+template <int NT, int C>
+__device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n, int k,
+                                                uint32_t *hist, SelScratch &ss,
+                                                TopKOrder<C> &ord) {
+    const int tid = threadIdx.x, lane = lane_id(), wid = wave_id();
+    if constexpr (C * NT <= 8192) {
+        // Few keys: bits 30..20, 19..9 and 8..0 over 2048-, 2048- and 512-bin
+        // histograms.
+        uint32_t *g1 = hist, *g2 = hist + 2048, *g3 = hist + 4096;
+        for (int i = tid; i < (4096 + 512) / 4; i += NT)
+            reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
+        __syncthreads();
+        int kk = k, bucket;
+        uint32_t d1, d2, d3;
+        narrow_pass<NT, C, 2048>(key, n, 20, 0, g1, ss, kk, bucket, d1);
+        SelRule rule{d1 << 20, n};
+        if (kk < bucket) {
+            narrow_pass<NT, C, 2048>(key, n, 9, d1, g2, ss, kk, bucket, d2);
+            rule.v = (d1 << 20) | (d2 << 9);
+            if (kk < bucket) {
+                narrow_pass<NT, C, 512>(key, n, 0, (d1 << 11) | d2, g3, ss, kk, bucket, d3);
+                rule.v |= d3;
+                if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, rule.v, kk, ord, ss);
+            }
+        }
+        topk_table<NT, C>(key, n, rule, ord);
+        return;
+    }
+    uint32_t *h1 = hist, *h2 = hist + kSelPadWords, *h3 = h2 + 2048;
+    for (int i = tid; i < kSelHistF32Words / 4; i += NT)
+        reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < C; ++r) atomicAdd(&h1[hist_pad(key[r] >> 17)], 1u);
+    if (tid == 0 && n < C * NT) atomicSub(&h1[0], (uint32_t)(C * NT - n));   // the items past n
+    __syncthreads();
+    uint32_t d1;
+    int kk, bucket;
+    find_digit<16384, false>(h1, k, ss, d1, kk, bucket);
+    SelRule rule{d1 << 17, n};
+    if (kk < bucket) {
+        // Items past n hold key 0: their lanes are masked only when the bin
+        // found so far is the one holding 0.
+        const uint32_t lo = d1 << 17;
+        if (lo == 0) {
+#pragma unroll
+            for (int r = 0; r < C; ++r) {
+                const uint64_t bc = __ballot(key[r] < (1u << 17)) & lanes_valid<NT>(r, wid, n);
+                if ((bc >> lane) & 1) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < C; ++r)
+                if (key[r] - lo < (1u << 17)) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
+        }
+        __syncthreads();
+        uint32_t d2;
+        find_digit<2048, false>(h2, kk, ss, d2, kk, bucket);
+        uint32_t v = lo | (d2 << 6);
+        if (kk < bucket) {
+            if (v == 0) {
+#pragma unroll
+                for (int r = 0; r < C; ++r) {
+                    const uint64_t bc = __ballot(key[r] < 64u) & lanes_valid<NT>(r, wid, n);
+                    if ((bc >> lane) & 1) atomicAdd(&h3[key[r] & 63u], 1u);
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < C; ++r)
+                    if (key[r] - v < 64u) atomicAdd(&h3[key[r] & 63u], 1u);
+            }
+            __syncthreads();
+            uint32_t d3;
+            find_digit<64, false>(h3, kk, ss, d3, kk, bucket);
+            v |= d3;
+        }
+        rule = SelRule{v, n};
+        if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, v, kk, ord, ss);
+    }
+    topk_table<NT, C>(key, n, rule, ord);
 }
 
 // Ascending position (among the selected) of this thread's selected item r.
@@ -410,31 +459,6 @@ template <int C>
 __device__ __forceinline__ int topk_pos(const TopKOrder<C> &ord, int r) {
     const int wid = threadIdx.x / kWave;
     return ord.off[r * kMaxBlockWaves + wid] + (int)lanes_below(ord.sel[r][wid]);
-}
-
-// Index of the selected item at ascending position p (0 <= p < number
-// selected), any thread: binary search of the scanned table, then the
-// position's set bit in that (row, wave) ballot.
-template <int NT, int C>
-__device__ __forceinline__ int topk_item_at(const TopKOrder<C> &ord, int p) {
-    constexpr int E = C * kMaxBlockWaves;
-    int lo = 0, hi = E - 1;   // largest e with off[e] <= p holds p
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (ord.off[mid] <= p) lo = mid; else hi = mid - 1;
-    }
-    const int r = lo / kMaxBlockWaves, w = lo % kMaxBlockWaves;
-    uint64_t m = ord.sel[r][w];
-    int n = p - ord.off[lo];   // the n-th set bit (from 0) of m
-    int base = 0;
-#pragma unroll
-    for (int half = 32; half >= 1; half >>= 1) {
-        const uint64_t lowmask = (half == 64) ? ~0ull : ((1ull << half) - 1);
-        const int cnt = __popcll(m & lowmask);
-        if (n >= cnt) { n -= cnt; m >>= half; base += half; }
-        else m &= lowmask;
-    }
-    return r * NT + w * kWave + base;
 }
 
 // Whether item i (0 <= i < C * NT) is selected, any thread.

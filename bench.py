@@ -53,7 +53,12 @@ def parse():
                     help="measure the proxy-cost ratio alpha (quantised over 16-bit proxy)")
     ap.add_argument("--calib-tokens", type=int, default=32,
                     help="held-out synthetic vectors for the threshold calibration")
-    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--cpu-budget-s", type=float, default=10.0,
+                    help="seconds of sparse oracle calls (the dense oracle gets half)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (c1, c2, c3 batch 1/4/16, c5 stack)")
+    ap.add_argument("--config-steps", type=int, default=20,
+                    help="timed calls per workload in the configs object")
     ap.add_argument("--warm", action="store_true", help="headline from back-to-back calls")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 5 times (reference kernel of known "
@@ -249,7 +254,7 @@ def main():
     total_bytes = sum(ab.values())
     med = statistics.median(cold_us)
     mean = statistics.mean(cold_us)
-    gbs = total_bytes / (mean * 1e-6) / 1e9
+    gbs = total_bytes / (med * 1e-6) / 1e9   # every rate and ratio below uses the median
 
     # Dominant kernel: the fused Stage 2 kernel (three kept rows of d
     # elements per kept channel, plus the f proxy scores it ranks).
@@ -276,6 +281,16 @@ def main():
     if not args.no_cpu:
         cpu = cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes)
 
+    torch_dense = None
+    if not args.no_dense:
+        torch_dense = torch_dense_leg(args, w, xs, n_x, flush, sink, torch)
+
+    configs = None
+    if not args.no_configs and args.batch is None and args.ffn_sparsity is None:
+        del w, proxy, flush
+        torch.cuda.empty_cache()
+        configs = config_legs(args, np, torch, prox, W, dev)
+
     s1 = 1 - k_in / cfg.d_model
     s2 = 1 - k_ff / cfg.d_ff
     out = {
@@ -300,7 +315,8 @@ def main():
                         "p10": round(pct(cold_us, 0.1), 2), "p90": round(pct(cold_us, 0.9), 2),
                         "warm_back_to_back": round(warm_us, 2),
                         "protocol": "warm" if args.warm else "cold (1 GiB read between calls evicts the caches)"},
-        "tokens_per_s": round(1e6 / mean, 1),
+        "statistic": "median of per-call HIP-event times (value, hbm_frac, tokens_per_s, speedup_vs_dense); ms_per_step is the mean",
+        "tokens_per_s": round(1e6 / med, 1),
         "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
         "algorithmic_bytes": total_bytes,
         "stage_us": {k: round(v, 2) for k, v in stage_us.items()},
@@ -313,6 +329,8 @@ def main():
         "cpu_baseline": cpu,
         "threshold_mode": tau,
         "w4a16": w4,
+        "torch_dense": torch_dense,
+        "configs": configs,
     }
     print(json.dumps(out), flush=True)
 
@@ -461,23 +479,180 @@ def bench_alpha(args, np, torch, prox, W, dev):
 
 def cpu_baseline(args, cfg, wl, xs_np, B, k_in, k_ff, total_bytes):
     """The CPU oracle as it stands, timed on this host on a bounded sample of
-    the same workload (proxy quantised once beforehand, untimed)."""
+    the same workload (proxy quantised once beforehand, untimed): sparse calls
+    for the budget, then dense calls for half of it."""
     import oracle
     cg, sg = oracle.quantize(wl.w_gate, cfg.dtype, cfg.qbits, cfg.group)
     cu, su = oracle.quantize(wl.w_up, cfg.dtype, cfg.qbits, cfg.group)
-    n = 0
-    t0 = time.perf_counter()
-    # Calls on the bench's decode vectors in turn until the time budget is spent.
-    while (time.perf_counter() - t0) < args.cpu_budget_s:
-        oracle.ffn_sparse(xs_np[n % len(xs_np)], cfg.dtype, wl.w_gate, wl.w_up, wl.w_down, k_in,
-                          k_ff, codes_g=cg, scales_g=sg, codes_u=cu, scales_u=su, group=cfg.group)
-        n += 1
-    dt = (time.perf_counter() - t0) / max(n, 1)
+
+    def run(fn, budget):
+        n = 0
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) < budget:   # decode vectors in turn
+            fn(xs_np[n % len(xs_np)])
+            n += 1
+        return (time.perf_counter() - t0) / max(n, 1), n, time.perf_counter() - t0
+
+    dt, n, spent = run(lambda x: oracle.ffn_sparse(x, cfg.dtype, wl.w_gate, wl.w_up, wl.w_down,
+                                                   k_in, k_ff, codes_g=cg, scales_g=sg,
+                                                   codes_u=cu, scales_u=su, group=cfg.group),
+                       args.cpu_budget_s)
+    ddt, dn, dspent = run(lambda x: oracle.ffn_dense(x, cfg.dtype, wl.w_gate, wl.w_up,
+                                                     wl.w_down), args.cpu_budget_s / 2)
     return {"value": round(total_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
-            "kind": "oracle", "us_per_call": round(dt * 1e6, 1),
-            "sample": f"{n} sparse decode calls of {cfg.name} at batch {B} over "
-                      f"{min(n, len(xs_np))} decode vectors, {time.perf_counter() - t0:.1f} s "
-                      f"(fp64 C oracle, OpenMP; proxy quantised beforehand)"}
+            "nproc": os.cpu_count(), "kind": "oracle", "us_per_call": round(dt * 1e6, 1),
+            "dense_us_per_call": round(ddt * 1e6, 1),
+            "sample": f"{n} sparse decode calls ({spent:.1f} s) and {dn} dense calls "
+                      f"({dspent:.1f} s) of {cfg.name} at batch {B} over the bench's decode "
+                      f"vectors (fp64 C oracle, OpenMP; proxy quantised beforehand)"}
+
+
+def torch_dense_leg(args, w, xs, n_x, flush, sink, torch):
+    """A dense FFN through torch (hipBLASLt GEMVs: F.linear for gate and up,
+    SiLU product, matmul for down), timed like the HIP dense FFN: a check that
+    the dense baseline of the speedup is competitive."""
+    import torch.nn.functional as F
+
+    def call(i):
+        x = xs[i % n_x]
+        h = F.silu(F.linear(x, w.w_gate)) * F.linear(x, w.w_up)
+        return torch.matmul(h, w.w_down)
+
+    for i in range(args.warmup):
+        call(i)
+    us = []
+    for i in range(args.steps):
+        torch.sum(flush, 0, out=sink)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        call(i)
+        b.record()
+        us.append((a, b))
+    torch.cuda.synchronize()
+    v = [a.elapsed_time(b) * 1e3 for a, b in us]
+    return {"us_per_call": round(statistics.median(v), 2),
+            "what": "torch bf16 F.linear(x, W_gate), F.linear(x, W_up), SiLU product, "
+                    "matmul with W_down; cold, median"}
+
+
+def timed_calls(fn, n, flush, sink, torch, cold=True):
+    """Per-call HIP-event times (µs) of n calls, each after a 1 GiB cache flush."""
+    evs = []
+    for i in range(n):
+        if cold:
+            torch.sum(flush, 0, out=sink)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn(i)
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) * 1e3 for a, b in evs]
+
+
+def config_legs(args, np, torch, prox, W, dev):
+    """The other synthetic workloads, each timed cold like the headline (median
+    of --config-steps calls) next to the dense HIP FFN: C1, C2, C3 at 70% FFN
+    sparsity and batch 1, 4, 16, and the 36-layer C5 stack per token."""
+    flush = torch.ones(FLUSH_BYTES // 8, dtype=torch.int64, device=dev)
+    sink = torch.zeros((), dtype=torch.int64, device=dev)
+    n = args.config_steps
+    out = {}
+    runs = [("c1_1024x3072_f16", 1), ("c2_4096x12288_bf16", 1), ("c3_4096x14336_bf16", 1),
+            ("c3_4096x14336_bf16", 4), ("c3_4096x14336_bf16", 16)]
+    loaded = {}
+    for name, B in runs:
+        cfg = W.CONFIGS[name]
+        if name not in loaded:
+            loaded.clear()
+            torch.cuda.empty_cache()
+            wl = W.make_workload(cfg)
+            w = prox.Weights(*(prox.from_bits(m, cfg.dtype, dev)
+                               for m in (wl.w_gate, wl.w_up, wl.w_down)))
+            p = prox.pack_proxy(w, prox.INT4 if cfg.qbits == 4 else prox.INT8, cfg.group)
+            loaded[name] = (wl, w, p)
+        wl, w, p = loaded[name]
+        k_ff = W.frac_to_k(0.3, cfg.d_ff) if name.startswith("c3") else cfg.k_ff
+        n_x = 8
+        xs = prox.from_bits(wl.x_vectors(n_x, B).reshape(n_x, B * cfg.d_model), cfg.dtype,
+                            dev).view(n_x, B, cfg.d_model)
+        ws = prox.new_workspace(cfg.d_model, cfg.d_ff, B, dev)
+        y = torch.empty((B, cfg.d_model), dtype=w.dtype, device=dev)
+        mask = torch.empty(cfg.d_ff, dtype=torch.uint8, device=dev)
+
+        def sparse(i):
+            prox.ffn_sparse(w, p, xs[i % n_x], cfg.k_in, k_ff, y=y, mask=mask, ws=ws)
+
+        def dense(i):
+            prox.ffn_dense(w, xs[i % n_x], y=y, ws=ws)
+
+        for i in range(args.warmup):
+            sparse(i)
+            dense(i)
+        su = statistics.median(timed_calls(sparse, n, flush, sink, torch))
+        du = statistics.median(timed_calls(dense, n, flush, sink, torch))
+        byts = sum(algorithmic_bytes(cfg, B, cfg.k_in, k_ff).values())
+        out[f"{name}_b{B}"] = {
+            "d_model": cfg.d_model, "d_ff": cfg.d_ff, "batch": B, "k_in": cfg.k_in, "k_ff": k_ff,
+            "ffn_sparsity_s2": round(1 - k_ff / cfg.d_ff, 4),
+            "us_per_call": round(su, 2), "tokens_per_s": round(B * 1e6 / su, 1),
+            "algorithmic_bytes": byts, "gbs": round(byts / (su * 1e-6) / 1e9, 1),
+            "hbm_frac": round(byts / (su * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "dense_us_per_call": round(du, 2), "speedup_vs_dense": round(du / su, 3)}
+        del ws, xs
+    loaded.clear()
+    torch.cuda.empty_cache()
+    out["c5_stack36_4096x12288_bf16_b1"] = stack_leg(args, np, torch, prox, W, dev)
+    return out
+
+
+def stack_leg(args, np, torch, prox, W, dev):
+    """The 36-layer stack per token (prox_ffn_sparse then the residual RMSNorm
+    per layer, back to back on one stream), next to the dense stack."""
+    L = W.STACK_LAYERS
+    layers = []
+    for l in range(L):
+        cfg = W.stack_layer_config(l)
+        wl = W.make_workload(cfg)
+        w = prox.Weights(*(prox.from_bits(m, cfg.dtype, dev) for m in (wl.w_gate, wl.w_up, wl.w_down)))
+        layers.append((w, prox.pack_proxy(w, prox.INT4, cfg.group)))
+        del wl
+    cfg = W.stack_layer_config(0)
+    x0 = prox.from_bits(W.make_workload(cfg, weights=False).x_vectors(1, 1)[0], cfg.dtype, dev)
+    ws = prox.new_workspace(cfg.d_model, cfg.d_ff, 1, dev)
+    y, x = torch.empty_like(x0), torch.empty_like(x0)
+    mask = torch.empty(cfg.d_ff, dtype=torch.uint8, device=dev)
+
+    def token(dense=False):
+        x.copy_(x0)
+        for w, p in layers:
+            if dense:
+                prox.ffn_dense(w, x, y=y, ws=ws)
+            else:
+                prox.ffn_sparse(w, p, x, cfg.k_in, cfg.k_ff, y=y, mask=mask, ws=ws)
+            prox.add_rmsnorm(x, y, 1e-6, out=x)
+
+    def per_token(dense):
+        token(dense)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(args.config_steps):
+            token(dense)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / args.config_steps
+
+    su, du = per_token(False), per_token(True)
+    byts = sum(algorithmic_bytes(cfg, 1, cfg.k_in, cfg.k_ff).values()) * L
+    out = {"layers": L, "k_in": cfg.k_in, "k_ff": cfg.k_ff, "us_per_token": round(su, 1),
+           "tokens_per_s": round(1e6 / su, 1), "algorithmic_bytes_per_token": byts,
+           "gbs": round(byts / (su * 1e-6) / 1e9, 1),
+           "hbm_frac": round(byts / (su * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+           "dense_us_per_token": round(du, 1), "speedup_vs_dense": round(du / su, 3),
+           "protocol": "back-to-back tokens (12.7 GB of weights per token exceed the caches)"}
+    del layers
+    torch.cuda.empty_cache()
+    return out
 
 
 def bench_stack(args, np, torch, prox, W, dev):

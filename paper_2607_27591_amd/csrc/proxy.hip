@@ -79,8 +79,16 @@ __device__ __forceinline__ void int8_pair_fma8(uint2 a, uint2 b, uint32_t xpair,
 __host__ __device__ inline int proxy_list_cap(int k_in, int ng) {
     return (k_in + ng + 1) / 2 * 2;   // kept rows + one pad per odd group, even
 }
+__host__ __device__ inline size_t proxy_list_bytes(int k_in, int ng, int nbt) {
+    return align_up((size_t)proxy_list_cap(k_in, ng) * 2 * (1 + nbt), 16);
+}
+// One tile's scales, [ng][gate T | up T] fp16, follow the list.  With
+// proxy_max_nb rows per launch list and scales fit in every case (k_in <= d:
+// at most 115 KB at d = 8192 and 4 rows, 130 KB at d = 16384 and 1 row).
+__host__ __device__ inline size_t proxy_scale_bytes(int ng, int T) { return (size_t)ng * 2 * T * 2; }
+constexpr size_t kProxyDynLdsMax = 152 * 1024;   // the static tables take the rest
 __host__ __device__ inline size_t proxy_lds_bytes(int k_in, int ng, int nbt, int T) {
-    const size_t list = align_up((size_t)proxy_list_cap(k_in, ng) * 2 * (1 + nbt), 16);
+    const size_t list = proxy_list_bytes(k_in, ng, nbt) + proxy_scale_bytes(ng, T);
     const size_t red = (size_t)kMaxBlockWaves * nbt * 2 * T * 4;
     const size_t m = list > red ? list : red;
     return m > kSelHistU16Bytes ? m : kSelHistU16Bytes;   // the selection's histogram first
@@ -161,6 +169,26 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     uint16_t *rows_sh = reinterpret_cast<uint16_t *>(dsm);   // [cap]
     uint16_t *xs_sh = rows_sh + cap;                          // [NB][cap]
 
+    // This tile's scales go to LDS behind the list: loaded here, held in
+    // registers through the input selection, stored once its histogram is
+    // dead.  A group change in the stream then waits on LDS only, never on
+    // the global loads in flight.
+    uint16_t *sc_sh = reinterpret_cast<uint16_t *>(dsm + proxy_list_bytes(k_in, ng, NB));
+    const uint4 *tsc = reinterpret_cast<const uint4 *>(
+        reinterpret_cast<const uint16_t *>(blob + L.scales_offset) + (size_t)tile * ng * 2 * T);
+    const int nsc4 = ng * T / 4;                         // uint4 of this tile's scales
+    constexpr int SPT = C * T / 512 > 1 ? C * T / 512 : 1;   // 1, 2 or 4 >= nsc4 / kBlock
+    static_assert(SPT == 1 || SPT == 2 || SPT == 4, "scale vectors per thread");
+    // Clamped indices keep every load in flight at once (a repeat stores the
+    // same value); named registers, as an array here went to scratch.
+    auto sc_idx = [&](int k) { return min(k * kBlock + tid, nsc4 - 1); };
+    uint4 scr0 = tsc[sc_idx(0)], scr1, scr2, scr3;
+    if constexpr (SPT > 1) scr1 = tsc[sc_idx(1)];
+    if constexpr (SPT > 2) {
+        scr2 = tsc[sc_idx(2)];
+        scr3 = tsc[sc_idx(3)];
+    }
+
     // ---- input top-k: item r of thread t is row r * kBlock + t ----
     // Key of row i: max over the batch of |x_i| as its 15-bit magnitude
     // pattern (monotone in |x| for fp16 and bf16, +0 and -0 equal).  Loads use
@@ -225,6 +253,16 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     }
     __syncthreads();
 
+    {
+        uint4 *sc4 = reinterpret_cast<uint4 *>(sc_sh);
+        sc4[sc_idx(0)] = scr0;
+        if constexpr (SPT > 1) sc4[sc_idx(1)] = scr1;
+        if constexpr (SPT > 2) {
+            sc4[sc_idx(2)] = scr2;
+            sc4[sc_idx(3)] = scr3;
+        }
+    }
+
     // ---- kept rows to their padded list positions (x as bf16/fp16 bits) ----
     // The 64 inputs of a (row, wave) share one quantisation group (group is a
     // multiple of 128), so a kept input's list position is its group's padded
@@ -282,8 +320,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
 
     // ---- stream the kept row pairs: lane group l owns a contiguous range ----
     // Per group the lane accumulates x_a (M + n_a) + x_b (M + n_b) and the x
-    // sum; at a group change acc - (M + 8) * xsum is scaled into tot.  The
-    // next group's scales are prefetched, so the stream never drains.
+    // sum; at a group change acc - (M + 8) * xsum is scaled into tot.
     const int npairs = gstart[ng] / 2;
     const int lgi = wid * NGRP + lane / LPS;
     const int pa = (int)((long long)lgi * npairs / NLG);
@@ -296,9 +333,6 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     const uint8_t *tbase = blob + L.codes_offset + (size_t)tile * L.row_bytes;
     const uint32_t rstride = (uint32_t)L.row_stride;   // < 2^24: 24-bit multiplies
     const uint32_t lane_off = (uint32_t)(mat * (T * QB / 8) + colc * QB / 8);
-    const uint4 *sbase = reinterpret_cast<const uint4 *>(
-        reinterpret_cast<const uint16_t *>(blob + L.scales_offset) + (size_t)tile * ng * 2 * T +
-        (size_t)mat * T + colc);
 
     float tot[NB][CPL];
 #pragma unroll
@@ -310,11 +344,13 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         int g = 0;
         while (gstart[g + 1] / 2 <= pa) ++g;
         int gend = gstart[g + 1] / 2;
-        uint4 sc[SZ], scn[SZ];
+        uint4 sc[SZ];
+        auto load_sc = [&](int gg) {
+            const uint4 *q = reinterpret_cast<const uint4 *>(sc_sh + (size_t)gg * 2 * T + mat * T + colc);
 #pragma unroll
-        for (int z = 0; z < SZ; ++z) sc[z] = sbase[(size_t)g * (T / 4) + z];
-#pragma unroll
-        for (int z = 0; z < SZ; ++z) scn[z] = sbase[(size_t)min(g + 1, ng - 1) * (T / 4) + z];
+            for (int z = 0; z < SZ; ++z) sc[z] = q[z];
+        };
+        load_sc(g);
         float acc[NB][CPL], xs[NB];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
@@ -360,17 +396,8 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                 {
                     if (p < pb && p >= gend) {
                         flush();
-                        const int gp = g;
                         do { ++g; } while (gstart[g + 1] / 2 <= p);
-                        if (g == gp + 1) {
-#pragma unroll
-                            for (int z = 0; z < SZ; ++z) sc[z] = scn[z];
-                        } else {
-#pragma unroll
-                            for (int z = 0; z < SZ; ++z) sc[z] = sbase[(size_t)g * (T / 4) + z];
-                        }
-#pragma unroll
-                        for (int z = 0; z < SZ; ++z) scn[z] = sbase[(size_t)min(g + 1, ng - 1) * (T / 4) + z];
+                        load_sc(g);
                         gend = gstart[g + 1] / 2;
                     }
 #pragma unroll
@@ -433,6 +460,7 @@ static hipError_t launch_proxy_t(const void *x_all, int B_all, int row0, int nb,
                                  uint8_t *in_mask, float *scores, int accumulate, Select sel_rule, int act, hipStream_t s) {
     const BlobLayout L(d, f, QB, group);
     const size_t lds = proxy_lds_bytes(k_in, d / group, NB, T);
+    if (lds > kProxyDynLdsMax) return hipErrorInvalidValue;   // excluded by proxy_max_nb
     if (lds > 65536) {
         const hipError_t e = hipFuncSetAttribute(
             reinterpret_cast<const void *>(proxy_kernel<NB, DT, QB, T, C>),
@@ -479,7 +507,7 @@ static hipError_t launch_proxy_tile(const void *x_all, int B_all, int row0, int 
     return launch_proxy_nb<DT, QB, 64>(x_all, B_all, row0, nb, d, f, group, k_in, blob, in_mask, scores, accumulate, sel_rule, act, s);
 }
 
-int proxy_max_nb(int d) { return d <= 8192 ? kProxyMaxNB : 2; }
+int proxy_max_nb(int d) { return d <= 8192 ? kProxyMaxNB : 1; }
 
 hipError_t launch_proxy(int dtype, int qbits, const void *x_all, int B_all, int row0, int nb,
                         int d, int f, int group, int k_in, const void *blob,

@@ -58,7 +58,7 @@ SMALL = {
                                                   in_frac=0.4, sigma_w=0.02, n_outliers=8),
     "bf16_i4_perrow_2048x1200_b6": W.small_config(d=2048, f=1200, batch=6, seed=22, group=2048,
                                                   in_frac=0.4, sigma_w=0.02),
-    # Maximum sizes: d_model 16384 (16 input rows per thread, 2 batch rows
+    # Maximum sizes: d_model 16384 (16 input rows per thread, 1 batch row
     # per proxy launch) and d_ff 65536 (64 score rows per thread).
     "bf16_i4_16384x320_b3": W.small_config(d=16384, f=320, batch=3, seed=10, in_frac=0.3,
                                            sigma_w=0.01),

@@ -32,7 +32,16 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* The enums are int-sized.  In C++ they get int as their fixed underlying
+ * type, so any int a C caller passes is a valid value there too (the entry
+ * points reject the ones outside the enumerators). */
+#ifdef __cplusplus
+#define PROX_ENUM_INT : int
+#else
+#define PROX_ENUM_INT
+#endif
+
+typedef enum PROX_ENUM_INT {
     PROX_OK = 0,
     PROX_ERR_INVALID = 1,     /* null pointer, size out of range, misalignment */
     PROX_ERR_UNSUPPORTED = 2, /* well-formed but outside the supported shapes */
@@ -40,19 +49,19 @@ typedef enum {
     PROX_ERR_HIP = 4          /* a HIP launch or runtime call failed */
 } prox_status;
 
-typedef enum { PROX_F16 = 0, PROX_BF16 = 1 } prox_dtype;
+typedef enum PROX_ENUM_INT { PROX_F16 = 0, PROX_BF16 = 1 } prox_dtype;
 
 /* Gate activation: SwiGLU (SiLU(z) = z / (1 + e^-z), Sec. 2.1) or GeGLU
  * (GELU(z) = z * Phi(z) = z (1 + erf(z / sqrt 2)) / 2, the gated FFN of the
  * Gemma models the paper mentions).  Applied to the proxy (Stage 1) and to
  * the exact gate (Stage 2) alike. */
-typedef enum { PROX_ACT_SILU = 0, PROX_ACT_GELU = 1 } prox_act;
+typedef enum PROX_ENUM_INT { PROX_ACT_SILU = 0, PROX_ACT_GELU = 1 } prox_act;
 
 /* Proxy formats.  PROX_Q_NONE keeps W_gate, W_up themselves, in the weights'
  * 16-bit dtype (the unquantised-proxy ablation, W~ = W; also the reference
  * point of the proxy-cost ratio alpha of Sec. 4.2); it takes group = d_model
  * and has no codes to unpack. */
-typedef enum { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1, PROX_Q_NONE = 2 } prox_qfmt;
+typedef enum PROX_ENUM_INT { PROX_Q_INT8 = 0, PROX_Q_INT4 = 1, PROX_Q_NONE = 2 } prox_qfmt;
 
 /* Supported sizes.  Batches past the rows one launch takes (Stage 1: 4 on the
  * dot-product kernel, 8 or 16 on the matrix cores; Stage 2: 16 per chunk on

@@ -12,8 +12,11 @@
 // 2^15 values of a 16-bit magnitude (two 16-bit counters per word), or, for
 // fp32 scores, passes over bits 30..17 of every key, then bits 16..6 and 5..0
 // of the keys that match the digits found so far, ending as soon as the found
-// bin is wholly in the top k.  A pass is one round of LDS atomics and a
-// block-wide scan of the bin counts from the top.  Ties at the k-th key are
+// bin is wholly in the top k.  Small blocks (at most 4096 items of 16-bit
+// keys, 8192 scores) take narrow passes instead, whose scans are cheaper than
+// the items they add: 8 + 7 bits for 16-bit keys, 11 + 11 + 9 for scores.  A
+// pass is one round of LDS atomics and a block-wide scan of the bin counts
+// from the top.  Ties at the k-th key are
 // cut by index: of the keys equal to it, those up to the index of the needed
 // one are in.  The selection then costs one or two compares per item: each
 // wave keeps the ballots of its rows (TopKOrder), and one scan of their

@@ -26,6 +26,22 @@ def _declared():
     return sorted(set(re.findall(r"\b(prox_[a-z_]+)\s*\(", text)))
 
 
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_as_c_and_cxx(tmp_path, lang):
+    # The boundary is a C header: a C11 and a C++17 translation unit both take
+    # it, and in C++ an out-of-range enum value (which C callers may pass) is a
+    # valid value of the enum's fixed int type.
+    comp = {"c": ["gcc", "-std=c11"], "c++": ["g++", "-std=c++17"]}[lang]
+    src = tmp_path / ("t.c" if lang == "c" else "t.cpp")
+    src.write_text('#include "prox.h"\n'
+                   'int main(void) { prox_qfmt f = (prox_qfmt)7; prox_dtype t = PROX_BF16;\n'
+                   '  return (int)f + (int)t + (int)sizeof(prox_status); }\n')
+    r = subprocess.run([*comp, "-fsyntax-only", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        "-I", os.path.dirname(HEADER), "-I", "/opt/rocm/include", str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
 def test_header_declares_the_boundary():
     names = _declared()
     for must in ["prox_pack_proxy", "prox_ffn_dense", "prox_ffn_sparse", "prox_ffn_sparse_tau",

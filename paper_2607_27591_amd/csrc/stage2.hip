@@ -128,19 +128,29 @@ __device__ __forceinline__ int stage2_slice(const float *__restrict__ scores, in
         } else {
             topk_select_f32<kBlock, C>(key, f, k_ff, hist, ss, ord);
         }
-        // This workgroup's slice of positions and its chunk of the mask,
-        // straight from the order tables: the thread of every (row, wave)
-        // entry whose kept channels meet [p0, p1) writes them in order.
-        if (tid < C * kMaxBlockWaves) {
-            int pos = ord.off[tid];
-            uint64_t m = ord.sel[tid / kMaxBlockWaves][tid % kMaxBlockWaves];
-            if (pos < p1 && pos + __popcll(m) > p0) {
-                const int j0 = (tid / kMaxBlockWaves) * kBlock + (tid % kMaxBlockWaves) * kWave;
-                for (; m; m &= m - 1, ++pos) {
-                    if (pos < p0 || pos >= p1) continue;
-                    const int j = min(j0 + __builtin_ctzll(m), f - 1);   // rows in bounds
-                    list[pos - p0] = j;
-                    if (klist_mode == kListWrite) klist[pos] = j;
+        // This workgroup's slice of positions straight from the order tables.
+        // The (row, wave) entry holding position p0 is found by one thread;
+        // then wave v expands entries e0 + v, e0 + v + 16, ... lane by lane
+        // (lane l: bit l of the entry's ballot, its position by a lane count)
+        // until the entries pass p1.
+        if (n > 0) {
+            if (tid < C * kMaxBlockWaves) {
+                const int pos = ord.off[tid];
+                const int cnt = __popcll(ord.sel[tid / kMaxBlockWaves][tid % kMaxBlockWaves]);
+                if (pos <= p0 && p0 < pos + cnt) ss.pick[0] = tid;   // exactly one entry
+            }
+            __syncthreads();
+            const int wid = wave_id(), lane = lane_id();
+            for (int e = ss.pick[0] + wid; e < C * kMaxBlockWaves; e += kMaxBlockWaves) {
+                const int pos = ord.off[e];   // wave-uniform
+                if (pos >= p1) break;
+                const uint64_t m = ord.sel[e / kMaxBlockWaves][e % kMaxBlockWaves];
+                const int q = pos + (int)lanes_below(m);
+                if (((m >> lane) & 1) && q >= p0 && q < p1) {
+                    const int j = min((e / kMaxBlockWaves) * kBlock + (e % kMaxBlockWaves) * kWave + lane,
+                                      f - 1);   // rows in bounds
+                    list[q - p0] = j;
+                    if (klist_mode == kListWrite) klist[q] = j;
                 }
             }
         }
@@ -194,40 +204,68 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     // | s [slice][NB].
     extern __shared__ __align__(16) float dyn[];
 
+    // x (when it goes to LDS) is loaded before the selection, so its load
+    // latency hides behind the ranking, and stored once the selection's
+    // histogram is dead; with 64 score rows per thread the registers are
+    // short, and x is loaded after it.  Thread t holds uint4 number
+    // k * kBlock + t of the [NB][d / 8] vectors.
+    const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
+    const int nvec = d / 8;
+    constexpr int XPT = NB * kMaxDModel / 8 / kBlock < 4 ? NB * kMaxDModel / 8 / kBlock : 4;
+    static_assert(XPT * kBlock * 8 >= 32768 || XPT * kBlock * 8 >= NB * kMaxDModel,
+                  "x vectors per thread cover every x that fits in LDS");
+    constexpr bool kEarlyX = C <= 32;
+    uint4 xr[XPT];
+    auto load_x = [&]() {
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int e = k * kBlock + tid, b = e / nvec;
+            xr[k] = xl && e < NB * nvec && b < nb
+                        ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[e % nvec]
+                        : make_uint4(0, 0, 0, 0);
+        }
+    };
+    if constexpr (kEarlyX) load_x();
+
     int p0;
     const int n = stage2_slice<C>(scores, f, k_ff, mask, scores_copy, sel_rule, klist,
                                   klist_mode, reinterpret_cast<uint32_t *>(dyn), ss, ord,
                                   sm.list, p0);
     (void)p0;
+    if constexpr (!kEarlyX) load_x();
 
-    const bool xl = x_in_lds(d, NB);   // always true with INT4 weights (host-checked)
     uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
-    const int nvec = d / 8;
     float *xsum = dyn + (size_t)NB * d / 2;   // INT4: [NB][d / 32] sums of x
     if constexpr (WQ == 4) {
         // x as pairs (x_{8m+k}, x_{8m+k+4}), k = 0..3, one uint4 per 8
         // inputs: nibble k of a code word and nibble k + 4 sit in the low and
         // high halves of (word >> 4k) & 0x000F000F, so one dot2 takes both.
-        for (int e = tid; e < NB * nvec; e += kBlock) {
-            const int b = e / nvec, vv = e % nvec;
-            const uint4 v = b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv]
-                                   : make_uint4(0, 0, 0, 0);
-            reinterpret_cast<uint4 *>(xs)[e] = make_uint4(
-                __builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
-                __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u));
-        }
-        for (int e = tid; e < NB * (d / 32); e += kBlock) {
-            const int b = e / (d / 32), c = e % (d / 32);
+        // The sum of every 32 inputs: 8 per lane in order, then the four
+        // lanes of a 32-input run (consecutive threads) as (s0 + s1) + (s2 + s3).
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int e = k * kBlock + tid;
+            const uint4 v = xr[k];
+            if (e < NB * nvec)
+                reinterpret_cast<uint4 *>(xs)[e] = make_uint4(
+                    __builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
+                    __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u));
+            const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
             float sum = 0.0f;
-            if (b < nb)
-                for (int k = 0; k < 32; ++k) sum += half_to_float<DT>(x[(size_t)b * d + c * 32 + k]);
-            xsum[e] = sum;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                sum += lo_to_float<DT>(vw[q]);
+                sum += hi_to_float<DT>(vw[q]);
+            }
+            sum += dpp_move<kDppXor1>(sum);
+            sum += dpp_move<kDppXor2>(sum);
+            if (e < NB * nvec && (tid & 3) == 0) xsum[e / 4] = sum;
         }
     } else if (xl) {
-        for (int e = tid; e < NB * nvec; e += kBlock) {
-            const int b = e / nvec, vv = e % nvec;
-            reinterpret_cast<uint4 *>(xs)[e] =
-                b < nb ? reinterpret_cast<const uint4 *>(x + (size_t)b * d)[vv] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int e = k * kBlock + tid;
+            if (e < NB * nvec) reinterpret_cast<uint4 *>(xs)[e] = xr[k];
         }
     }
     __syncthreads();

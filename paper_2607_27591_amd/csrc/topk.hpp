@@ -62,17 +62,6 @@ __device__ __forceinline__ int wave_id() {
     return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
 }
 
-// Lanes 0 .. m - 1 of a wave (all for m >= 64, none for m <= 0).
-__device__ __forceinline__ uint64_t lanes_first(int m) {
-    return m >= kWave ? ~0ull : m <= 0 ? 0ull : ((1ull << m) - 1);
-}
-
-// Lanes of wave wid whose item r * NT + tid is below n (wave-uniform).
-template <int NT>
-__device__ __forceinline__ uint64_t lanes_valid(int r, int wid, int n) {
-    return lanes_first(n - (r * NT + wid * kWave));
-}
-
 // v_writelane (lane `lane` of v replaced by the wave-uniform s) through its
 // LLVM intrinsic, so the compiler also inserts the wait states it needs
 // after the instruction that wrote s.
@@ -252,20 +241,20 @@ template <int NT, int C>
 __device__ __forceinline__ void topk_table(const uint32_t (&key)[C], int n, SelRule rule,
                                            TopKOrder<C> &ord) {
     const int wid = wave_id();
+    const int tid = threadIdx.x;
     // Items past n hold key 0, so only a rule that admits 0 needs their lanes
-    // masked.
+    // masked.  Index limits are per-lane compares inside the ballot (VALU),
+    // not wave masks built from shifts on the scalar unit, which the 16 waves
+    // of a CU share.
     const bool mask = rule.v == 0;
     if (rule.istar >= n) {
         store_ballots<C>(ord, wid, [&](int r) {
-            const uint64_t b = __ballot(key[r] >= rule.v);
-            return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+            return mask ? __ballot(key[r] >= rule.v && r * NT + tid < n) : __ballot(key[r] >= rule.v);
         });
     } else {
+        // istar < n: the index limit also keeps out the items past n.
         store_ballots<C>(ord, wid, [&](int r) {
-            const int base = r * NT + wid * kWave;   // index of lane 0 of this wave
-            const uint64_t b = __ballot(key[r] > rule.v) |
-                               (__ballot(key[r] == rule.v) & lanes_first(rule.istar - base + 1));
-            return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+            return __ballot(key[r] > rule.v || (key[r] == rule.v && r * NT + tid <= rule.istar));
         });
     }
     topk_scan_ballots<NT, C>(ord);
@@ -277,10 +266,10 @@ template <int NT, int C>
 __device__ __forceinline__ int topk_tie_index(const uint32_t (&key)[C], int n, uint32_t v,
                                               int need, TopKOrder<C> &ord, SelScratch &ss) {
     const int wid = wave_id();
+    const int tid = threadIdx.x;
     const bool mask = v == 0;   // items past n hold key 0
     store_ballots<C>(ord, wid, [&](int r) {
-        const uint64_t b = __ballot(key[r] == v);
-        return mask ? b & lanes_valid<NT>(r, wid, n) : b;
+        return mask ? __ballot(key[r] == v && r * NT + tid < n) : __ballot(key[r] == v);
     });
     topk_scan_ballots<NT, C>(ord);
     // The entry holding the need-th equal key (one thread finds it), then the
@@ -314,15 +303,14 @@ template <int NT, int C, int NBINS>
 __device__ __forceinline__ void narrow_pass(const uint32_t (&key)[C], int n, int shift,
                                             uint32_t prefix, uint32_t *h, SelScratch &ss,
                                             int &kk, int &bucket, uint32_t &digit) {
-    const int lane = lane_id(), wid = wave_id();
+    const int tid = threadIdx.x;
     constexpr uint32_t kMaskBins = NBINS - 1;
     const int top = shift + __builtin_ctz(NBINS);   // bits at or above top: the prefix
 #pragma unroll
     for (int r = 0; r < C; ++r) {
         // Keys past n are 0: masked whenever the prefix admits 0.
-        const bool match = top >= 32 || (key[r] >> top) == prefix;
-        const uint64_t b = __ballot(match) & (prefix == 0 ? lanes_valid<NT>(r, wid, n) : ~0ull);
-        if ((b >> lane) & 1) atomicAdd(&h[(key[r] >> shift) & kMaskBins], 1u);
+        const bool match = (top >= 32 || (key[r] >> top) == prefix) && (prefix != 0 || r * NT + tid < n);
+        if (match) atomicAdd(&h[(key[r] >> shift) & kMaskBins], 1u);
     }
     __syncthreads();
     find_digit<NBINS, false>(h, kk, ss, digit, kk, bucket);
@@ -379,7 +367,7 @@ template <int NT, int C>
 __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n, int k,
                                                 uint32_t *hist, SelScratch &ss,
                                                 TopKOrder<C> &ord) {
-    const int tid = threadIdx.x, lane = lane_id(), wid = wave_id();
+    const int tid = threadIdx.x;
     if constexpr (C * NT <= 8192) {
         // Few keys: bits 30..20, 19..9 and 8..0 over 2048-, 2048- and 512-bin
         // histograms.
@@ -421,10 +409,8 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
         const uint32_t lo = d1 << 17;
         if (lo == 0) {
 #pragma unroll
-            for (int r = 0; r < C; ++r) {
-                const uint64_t bc = __ballot(key[r] < (1u << 17)) & lanes_valid<NT>(r, wid, n);
-                if ((bc >> lane) & 1) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
-            }
+            for (int r = 0; r < C; ++r)
+                if (key[r] < (1u << 17) && r * NT + tid < n) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
         } else {
 #pragma unroll
             for (int r = 0; r < C; ++r)
@@ -437,10 +423,8 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
         if (kk < bucket) {
             if (v == 0) {
 #pragma unroll
-                for (int r = 0; r < C; ++r) {
-                    const uint64_t bc = __ballot(key[r] < 64u) & lanes_valid<NT>(r, wid, n);
-                    if ((bc >> lane) & 1) atomicAdd(&h3[key[r] & 63u], 1u);
-                }
+                for (int r = 0; r < C; ++r)
+                    if (key[r] < 64u && r * NT + tid < n) atomicAdd(&h3[key[r] & 63u], 1u);
             } else {
 #pragma unroll
                 for (int r = 0; r < C; ++r)

@@ -71,10 +71,11 @@ __device__ __forceinline__ uint32_t write_lane(uint32_t v, uint32_t s, int lane)
     return (uint32_t)prox_llvm_writelane((int)s, lane, (int)v);
 }
 
-// Every wave's row ballots to ord.sel: lane r of two registers takes row r's
-// ballot (lanes r < C), then one store per wave.
+// Every wave's row ballots to a [C][16] table (ord.sel, or another): lane r
+// of two registers takes row r's ballot (lanes r < C), then one store per
+// wave.
 template <int C, typename B>
-__device__ __forceinline__ void store_ballots(TopKOrder<C> &ord, int wid, B &&ballot_of_row) {
+__device__ __forceinline__ void store_ballots(uint64_t *table, int wid, B &&ballot_of_row) {
     uint32_t lo = 0, hi = 0;
 #pragma unroll
     for (int r = 0; r < C; ++r) {
@@ -83,7 +84,11 @@ __device__ __forceinline__ void store_ballots(TopKOrder<C> &ord, int wid, B &&ba
         hi = write_lane(hi, (uint32_t)(b >> 32), r);
     }
     const int lane = lane_id();
-    if (lane < C) ord.sel[lane][wid] = ((uint64_t)hi << 32) | lo;
+    if (lane < C) table[lane * kMaxBlockWaves + wid] = ((uint64_t)hi << 32) | lo;
+}
+template <int C, typename B>
+__device__ __forceinline__ void store_ballots(TopKOrder<C> &ord, int wid, B &&ballot_of_row) {
+    store_ballots<C>(&ord.sel[0][0], wid, ballot_of_row);
 }
 
 // Exclusive scan of the per-(row, wave) counts, taken as the popcounts of the
@@ -227,73 +232,69 @@ __device__ __forceinline__ void find_digit(const uint32_t *h, int kk, SelScratch
     bucket = ss.pick[2];
 }
 
-// The top-k rule once the threshold is known: every key above v is in; of the
-// keys equal to v, those with index <= istar (istar >= n: all of them).
-struct SelRule {
-    uint32_t v;
-    int istar;
-};
-
-// Order tables of `rule`: the ballot of every (row, wave) and, after one scan
-// of their popcounts, the exclusive prefix counts of the selected items in
-// index order.  Per item one compare, two for a tie cut.
+// Order tables of the rule "key >= v" (no tie to cut): the ballot of every
+// (row, wave) and, after one scan of their popcounts, the exclusive prefix
+// counts of the selected items in index order.  One compare per item; items
+// past n hold key 0, so only v = 0 needs an index limit, a per-lane compare
+// inside the ballot (VALU) rather than a wave mask built on the scalar unit,
+// which the 16 waves of a CU share.
 template <int NT, int C>
-__device__ __forceinline__ void topk_table(const uint32_t (&key)[C], int n, SelRule rule,
+__device__ __forceinline__ void topk_table(const uint32_t (&key)[C], int n, uint32_t v,
                                            TopKOrder<C> &ord) {
     const int wid = wave_id();
     const int tid = threadIdx.x;
-    // Items past n hold key 0, so only a rule that admits 0 needs their lanes
-    // masked.  Index limits are per-lane compares inside the ballot (VALU),
-    // not wave masks built from shifts on the scalar unit, which the 16 waves
-    // of a CU share.
-    const bool mask = rule.v == 0;
-    if (rule.istar >= n) {
-        store_ballots<C>(ord, wid, [&](int r) {
-            return mask ? __ballot(key[r] >= rule.v && r * NT + tid < n) : __ballot(key[r] >= rule.v);
-        });
-    } else {
-        // istar < n: the index limit also keeps out the items past n.
-        store_ballots<C>(ord, wid, [&](int r) {
-            return __ballot(key[r] > rule.v || (key[r] == rule.v && r * NT + tid <= rule.istar));
-        });
-    }
+    store_ballots<C>(ord, wid, [&](int r) {
+        return v == 0 ? __ballot(r * NT + tid < n) : __ballot(key[r] >= v);
+    });
     topk_scan_ballots<NT, C>(ord);
 }
 
-// Index of the need-th (from 1) key equal to v in index order; uses ord as
-// scratch (the caller rebuilds it afterwards).
+// Order tables of the top-k rule with a tie cut: every key above v is in, and
+// of the keys equal to v the first `need` in index order (0 < need < their
+// count).  The ballots of "above" and "equal" are scanned together (one
+// wave: exclusive prefixes G and Q per entry), the entry offsets are
+// G + min(need, Q), and each wave then ballots its final rows with the
+// equal-key rank Q + (equal lanes below) < need.  scratch: LDS words dead
+// after the last digit search, at least 3 C kMaxBlockWaves.
 template <int NT, int C>
-__device__ __forceinline__ int topk_tie_index(const uint32_t (&key)[C], int n, uint32_t v,
-                                              int need, TopKOrder<C> &ord, SelScratch &ss) {
-    const int wid = wave_id();
-    const int tid = threadIdx.x;
-    const bool mask = v == 0;   // items past n hold key 0
-    store_ballots<C>(ord, wid, [&](int r) {
-        return mask ? __ballot(key[r] == v && r * NT + tid < n) : __ballot(key[r] == v);
-    });
-    topk_scan_ballots<NT, C>(ord);
-    // The entry holding the need-th equal key (one thread finds it), then the
-    // set bit inside that entry's ballot.
-    const int e = threadIdx.x;
-    if (e < C * kMaxBlockWaves) {
-        const int before = ord.off[e];
-        uint64_t m = ord.sel[e / kMaxBlockWaves][e % kMaxBlockWaves];
-        if (before < need && need <= before + __popcll(m)) {
-            int q = need - 1 - before;   // the q-th set bit (from 0) of m
-            int bit = 0;
+__device__ __forceinline__ void topk_table_cut(const uint32_t (&key)[C], int n, uint32_t v,
+                                               int need, uint32_t *scratch, TopKOrder<C> &ord) {
+    static_assert(C % 4 == 0 && C * kMaxBlockWaves == kWave * (C / 4), "C / 4 entries per lane");
+    constexpr int E = C / 4;
+    const int wid = wave_id(), tid = threadIdx.x;
+    uint64_t *eqs = reinterpret_cast<uint64_t *>(scratch);    // [C][16] equal-key ballots
+    int *qpre = reinterpret_cast<int *>(eqs + C * kMaxBlockWaves);   // [C * 16] their prefixes
+    // Items past n hold key 0: they are never above v, and equal to it only
+    // when v = 0.
+    auto equal = [&](int r) { return key[r] == v && (v != 0 || r * NT + tid < n); };
+    store_ballots<C>(ord, wid, [&](int r) { return __ballot(key[r] > v); });
+    store_ballots<C>(eqs, wid, [&](int r) { return __ballot(equal(r)); });
+    __syncthreads();
+    if (tid < kWave) {
+        const int lane = lane_id();
+        const uint64_t *gt = &ord.sel[0][0];
+        int g[E], q[E], rg = 0, rq = 0;
 #pragma unroll
-            for (int half = 32; half >= 1; half >>= 1) {
-                const int c = __popcll(m & ((1ull << half) - 1));
-                if (q >= c) { q -= c; m >>= half; bit += half; }
-                else m &= (1ull << half) - 1;
-            }
-            ss.pick[0] = (e / kMaxBlockWaves) * NT + (e % kMaxBlockWaves) * kWave + bit;
+        for (int e = 0; e < E; ++e) {
+            g[e] = rg;
+            q[e] = rq;
+            rg += __popcll(gt[lane * E + e]);
+            rq += __popcll(eqs[lane * E + e]);
+        }
+        const int bg = wave_inclusive_scan(rg) - rg, bq = wave_inclusive_scan(rq) - rq;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            ord.off[lane * E + e] = bg + g[e] + min(need, bq + q[e]);
+            qpre[lane * E + e] = bq + q[e];
         }
     }
     __syncthreads();
-    const int istar = ss.pick[0];
-    __syncthreads();   // every thread has read ss.pick and ord
-    return istar;
+    store_ballots<C>(ord, wid, [&](int r) {
+        const bool eq = equal(r);
+        const int rank = qpre[r * kMaxBlockWaves + wid] + (int)lanes_below(__ballot(eq));
+        return __ballot(key[r] > v || (eq && rank < need));
+    });
+    __syncthreads();
 }
 
 // One narrow digit pass: counts bits [shift, shift + log2 NBINS) of the keys
@@ -334,13 +335,16 @@ __device__ __forceinline__ void topk_select_u15(const uint32_t (&key)[C], int n,
         int kk = k, bucket;
         uint32_t d1, d2;
         narrow_pass<NT, C, 256>(key, n, 7, 0, h1, ss, kk, bucket, d1);
-        SelRule rule{d1 << 7, n};
+        uint32_t v = d1 << 7;
         if (kk < bucket) {
             narrow_pass<NT, C, 128>(key, n, 0, d1, h2, ss, kk, bucket, d2);
-            rule.v = (d1 << 7) | d2;
-            if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, rule.v, kk, ord, ss);
+            v = (d1 << 7) | d2;
+            if (kk < bucket) {
+                topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
+                return;
+            }
         }
-        topk_table<NT, C>(key, n, rule, ord);
+        topk_table<NT, C>(key, n, v, ord);
         return;
     }
     for (int i = tid; i < kSelHistU16Words / 4; i += NT)
@@ -353,9 +357,8 @@ __device__ __forceinline__ void topk_select_u15(const uint32_t (&key)[C], int n,
     uint32_t v;
     int need, bucket;
     find_digit<32768, true>(hist, k, ss, v, need, bucket);
-    SelRule rule{v, n};
-    if (need < bucket) rule.istar = topk_tie_index<NT, C>(key, n, v, need, ord, ss);
-    topk_table<NT, C>(key, n, rule, ord);
+    if (need < bucket) topk_table_cut<NT, C>(key, n, v, need, hist, ord);
+    else topk_table<NT, C>(key, n, v, ord);
 }
 
 // Top k (1 <= k <= n) of non-negative fp32 keys (bit 31 clear): bits 30..17
@@ -378,17 +381,20 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
         int kk = k, bucket;
         uint32_t d1, d2, d3;
         narrow_pass<NT, C, 2048>(key, n, 20, 0, g1, ss, kk, bucket, d1);
-        SelRule rule{d1 << 20, n};
+        uint32_t v = d1 << 20;
         if (kk < bucket) {
             narrow_pass<NT, C, 2048>(key, n, 9, d1, g2, ss, kk, bucket, d2);
-            rule.v = (d1 << 20) | (d2 << 9);
+            v = (d1 << 20) | (d2 << 9);
             if (kk < bucket) {
                 narrow_pass<NT, C, 512>(key, n, 0, (d1 << 11) | d2, g3, ss, kk, bucket, d3);
-                rule.v |= d3;
-                if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, rule.v, kk, ord, ss);
+                v |= d3;
+                if (kk < bucket) {
+                    topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
+                    return;
+                }
             }
         }
-        topk_table<NT, C>(key, n, rule, ord);
+        topk_table<NT, C>(key, n, v, ord);
         return;
     }
     uint32_t *h1 = hist, *h2 = hist + kSelPadWords, *h3 = h2 + 2048;
@@ -402,7 +408,7 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
     uint32_t d1;
     int kk, bucket;
     find_digit<16384, false>(h1, k, ss, d1, kk, bucket);
-    SelRule rule{d1 << 17, n};
+    uint32_t thr = d1 << 17;
     if (kk < bucket) {
         // Items past n hold key 0: their lanes are masked only when the bin
         // found so far is the one holding 0.
@@ -435,10 +441,13 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
             find_digit<64, false>(h3, kk, ss, d3, kk, bucket);
             v |= d3;
         }
-        rule = SelRule{v, n};
-        if (kk < bucket) rule.istar = topk_tie_index<NT, C>(key, n, v, kk, ord, ss);
+        thr = v;
+        if (kk < bucket) {
+            topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
+            return;
+        }
     }
-    topk_table<NT, C>(key, n, rule, ord);
+    topk_table<NT, C>(key, n, thr, ord);
 }
 
 // Ascending position (among the selected) of this thread's selected item r.

@@ -237,18 +237,38 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         topk_select_u15<kBlock, C>(key, d, k_in, reinterpret_cast<uint32_t *>(dsm), ss, ord);
     }
 
-    // ---- group bookkeeping: kept rows per group and padded list starts ----
-    for (int g = tid; g <= ng; g += kBlock) gsel0[g] = topk_selected_before<kBlock, C>(ord, g * group);
-    __syncthreads();
+    // ---- group bookkeeping, one wave: kept rows before each group, padded
+    // list starts, and for every (row, wave) entry of the order tables the
+    // list position of its first kept input (into ord.off) ----
+    // The 64 inputs of an entry share one quantisation group (group is a
+    // multiple of 128), and a group boundary is an entry boundary, so the
+    // kept rows before it are that entry's offset.  i / group is a 32-bit
+    // reciprocal multiply: exact for i < 2^14 and group < 2^15 (the rounding
+    // error i * group / 2^32 stays below 1 / group).
+    const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;
     if (wid == 0) {
+        const int total = topk_selected_before<kBlock, C>(ord, C * kBlock);
+        auto before = [&](int gg) {
+            const int i = gg * group;
+            return i >= C * kBlock ? total : ord.off[(i / kBlock) * kMaxBlockWaves + (i % kBlock) / kWave];
+        };
         int carry = 0;
         for (int g0 = 0; g0 <= ng; g0 += kWave) {
             const int g = g0 + lane;
-            const int cnt = g < ng ? gsel0[g + 1] - gsel0[g] : 0;
+            const int s0 = g <= ng ? before(g) : 0;
+            const int cnt = g < ng ? before(g + 1) - s0 : 0;
             const int padded = (cnt + 1) / 2 * 2;
             const int incl = wave_inclusive_scan(padded);
-            if (g <= ng) gstart[g] = carry + incl - padded;
+            if (g <= ng) {
+                gsel0[g] = s0;
+                gstart[g] = carry + incl - padded;
+            }
             carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+        for (int e = lane; e < C * kMaxBlockWaves; e += kWave) {
+            const uint32_t i0 = (uint32_t)((e / kMaxBlockWaves) * kBlock + (e % kMaxBlockWaves) * kWave);
+            const int g = (int)__umulhi(i0, gmagic);
+            ord.off[e] += gstart[g] - gsel0[g];
         }
     }
     __syncthreads();
@@ -264,22 +284,16 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     }
 
     // ---- kept rows to their padded list positions (x as bf16/fp16 bits) ----
-    // The 64 inputs of a (row, wave) share one quantisation group (group is a
-    // multiple of 128), so a kept input's list position is its group's padded
-    // start plus its rank: wave-uniform table entries and a lane count.
-    // i / group as a 32-bit reciprocal multiply: exact for i < 2^14 and
-    // group < 2^15 (the rounding error i * group / 2^32 stays below 1 / group).
-    const uint32_t gmagic = 0xFFFFFFFFu / (uint32_t)group + 1u;
+    // A kept input's position: its entry's first position plus its rank in
+    // the entry (a lane count).
     const int swid = wave_id();
     int pos[C];   // list position of each of this thread's inputs, -1 if not kept
 #pragma unroll
     for (int r = 0; r < C; ++r) {
         const int i = r * kBlock + tid;
         const uint64_t bs = ord.sel[r][swid];
-        const int g = (int)__umulhi((uint32_t)(r * kBlock + swid * kWave), gmagic);
         const bool s = (bs >> lane) & 1;   // inputs past d are never kept
-        pos[r] = s ? gstart[g] - gsel0[g] + ord.off[r * kMaxBlockWaves + swid] + (int)lanes_below(bs)
-                   : -1;
+        pos[r] = s ? ord.off[r * kMaxBlockWaves + swid] + (int)lanes_below(bs) : -1;
         if (s) rows_sh[pos[r]] = (uint16_t)i;
     }
 #pragma unroll

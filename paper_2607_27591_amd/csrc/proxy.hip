@@ -11,14 +11,20 @@
 // padded per quantisation group to an even count.  Each lane group then
 // streams a contiguous range of row pairs.
 //
-// A lane reads 4 (INT4), 8 (INT8) or 16 (unquantised 16-bit proxy) bytes of
-// both rows' contiguous segments, i.e. the same 8 proxy columns of two input
-// rows.  For INT4 the two rows' bytes are interleaved with v_perm and each
-// nibble pair is OR-ed under the exponent of 128.0 (bf16) or 1024.0 (fp16):
-// that is the exact 16-bit pair (M + n_a, M + n_b), n = q + 8, and one dot2
-// accumulates x_a (M + n_a) + x_b (M + n_b) in fp32.  (M + 8) * sum(x) is
-// subtracted and the group's scale applied once per group, column and lane
-// group.  Lane groups and waves are summed in a fixed order, so results are
+// A lane reads 8 (INT4), 8 or 16 (INT8) or 16 (unquantised 16-bit proxy)
+// bytes of both rows' contiguous segments, i.e. the same proxy columns of two
+// input rows.  INT4 codes are dequantised in fp16 whatever the model dtype:
+// byte k of both rows goes side by side (one v_perm), its low nibble OR-ed
+// under the exponent of 1024.0 is the exact fp16 pair (1024 + n_a, 1024 + n_b),
+// n = q + 8, and its high nibble in place, with the same OR, is
+// (1024 + 16 n_a, 1024 + 16 n_b); one v_dot2_f32_f16 each accumulates
+// x_a (...) + x_b (...) in fp32.  Both nibbles of a byte need no shift, which
+// bf16 (7 mantissa bits) would.  The kept x go to the list in fp16: bf16 x are
+// scaled by one power of two 2^s that puts the largest |x| in [2^14, 2^15), so
+// every kept x is exact in fp16 down to 2^-28 of the largest, and the sums are
+// scaled back by 2^-s.  The code bias ((1024 + 8) or (1024 + 128) times sum(x))
+// is subtracted and the group's scale applied once per group, column and lane
+// group; high-nibble columns are divided by 16 at the end.  Lane groups and waves are summed in a fixed order, so results are
 // deterministic.  This kernel takes up to 4 batch rows per launch; five or
 // more rows with an INT4 proxy go to proxy_mfma_kernel (the matrix cores).
 #include "common.hpp"
@@ -41,24 +47,25 @@ __device__ __forceinline__ uint32_t and_or(uint32_t v, uint32_t mask, uint32_t b
     }
 }
 
-// acc[c] += x_a (M + n_a[c]) + x_b (M + n_b[c]) for the 8 INT4 columns held in
-// one 32-bit word of each row.
-template <int DT, bool FUSED>
-__device__ __forceinline__ void int4_pair_dot8(uint32_t a, uint32_t b, uint32_t xpair,
-                                               float *acc) {
-    constexpr uint32_t M = Int4Magic<DT>::pair;
-    constexpr uint32_t K = 0x000F000Fu;
-    const uint32_t p = __builtin_amdgcn_perm(b, a, 0x05040100u);  // a.b0 a.b1 b.b0 b.b1
-    const uint32_t q = __builtin_amdgcn_perm(b, a, 0x07060302u);  // a.b2 a.b3 b.b2 b.b3
-    acc[0] = dot2<DT>(xpair, and_or<FUSED>(p, K, M), acc[0]);
-    acc[1] = dot2<DT>(xpair, and_or<FUSED>(p >> 4, K, M), acc[1]);
-    acc[2] = dot2<DT>(xpair, and_or<FUSED>(p >> 8, K, M), acc[2]);
-    acc[3] = dot2<DT>(xpair, and_or<FUSED>(p >> 12, K, M), acc[3]);
-    acc[4] = dot2<DT>(xpair, and_or<FUSED>(q, K, M), acc[4]);
-    acc[5] = dot2<DT>(xpair, and_or<FUSED>(q >> 4, K, M), acc[5]);
-    acc[6] = dot2<DT>(xpair, and_or<FUSED>(q >> 8, K, M), acc[6]);
-    acc[7] = dot2<DT>(xpair, and_or<FUSED>(q >> 12, K, M), acc[7]);
+// acc[c] += x_a (1024 + n_a[c]) + x_b (1024 + n_b[c]) (even c) or
+// x_a (1024 + 16 n_a[c]) + x_b (1024 + 16 n_b[c]) (odd c) for the 8 INT4
+// columns of one 32-bit word of each row, x fp16: byte k of both words side by
+// side, then its low nibble (column 2k) or its high nibble in place (column
+// 2k + 1) OR-ed under the exponent of 1024.0, each exact in fp16.
+template <bool FUSED>
+__device__ __forceinline__ void int4_pair_dot8_h(uint32_t a, uint32_t b, uint32_t xpair,
+                                                 float *acc) {
+    constexpr uint32_t M = Int4Magic<kF16>::pair;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t p = __builtin_amdgcn_perm(b, a, (uint32_t)k | ((uint32_t)(k + 4) << 16));
+        acc[2 * k] = dot2<kF16>(xpair, and_or<FUSED>(p, 0x000F000Fu, M), acc[2 * k]);
+        acc[2 * k + 1] = dot2<kF16>(xpair, and_or<FUSED>(p, 0x00F000F0u, M), acc[2 * k + 1]);
+    }
 }
+// Code bias of column e of an fp16-dequantised INT4 word, and its scale.
+constexpr float kInt4HBias[2] = {1024.0f + 8.0f, 1024.0f + 128.0f};
+constexpr float kInt4HScale[2] = {1.0f, 1.0f / 16.0f};
 
 // acc[c] += x_a n_a[c] + x_b n_b[c] for 8 INT8 columns (n = q + 128).
 template <int DT>
@@ -116,10 +123,10 @@ __device__ __forceinline__ void pair_accumulate(const typename ProxyLoad<QB, CPL
                                                 const typename ProxyLoad<QB, CPL>::type &b,
                                                 uint32_t xp, float *acc) {
     if constexpr (QB == 4 && CPL == 16) {
-        int4_pair_dot8<DT, FUSED>(a.x, b.x, xp, acc);
-        int4_pair_dot8<DT, FUSED>(a.y, b.y, xp, acc + 8);
+        int4_pair_dot8_h<FUSED>(a.x, b.x, xp, acc);
+        int4_pair_dot8_h<FUSED>(a.y, b.y, xp, acc + 8);
     } else if constexpr (QB == 4) {
-        int4_pair_dot8<DT, FUSED>(a, b, xp, acc);
+        int4_pair_dot8_h<FUSED>(a, b, xp, acc);
     } else if constexpr (QB == 8 && CPL == 16) {
         int8_pair_fma8<DT>(make_uint2(a.x, a.y), make_uint2(b.x, b.y), xp, acc);
         int8_pair_fma8<DT>(make_uint2(a.z, a.w), make_uint2(b.z, b.w), xp, acc + 8);
@@ -152,7 +159,8 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
     constexpr int SZ = CPL / 8;                   // uint4 of scales per lane and group
     constexpr bool kEarlyX = NB <= 2;             // projected x loaded with the keys
     constexpr bool kHoistX = NB == 1;             // x pairs read with the code loads
-    constexpr float off = QB == 4 ? Int4Magic<DT>::offset : QB == 8 ? 128.0f : 0.0f;   // code bias
+    constexpr float off = QB == 8 ? 128.0f : 0.0f;   // code bias (INT4: per column, kInt4HBias)
+    constexpr bool kHx = QB == 4;                     // x in fp16 (INT4 codes dequantised in fp16)
     using W = typename ProxyLoad<QB, CPL>::type;
     const BlobLayout L(d, f, QB, group);
     const int tid = threadIdx.x, wid = tid / kWave, lane = lane_id();
@@ -221,6 +229,19 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
             }
         }
     }
+    // bf16 x for fp16-dequantised codes: the largest key sets the power of two
+    // that takes the kept x into fp16 (per wave here, across waves after the
+    // bookkeeping barrier; 15-bit magnitude patterns order like the values).
+    constexpr bool kScaleX = kHx && DT == kBF16;
+    __shared__ uint32_t wmax[kMaxBlockWaves];
+    if constexpr (kScaleX) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int r = 0; r < C; ++r) m = max(m, key[r]);
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o));
+        if (lane == 0) wmax[wid] = m;
+    }
     uint64_t sel = 0;
     if (sel_rule.tau_mode) {
         // Threshold rule: keep row i when max_b |x_{b,i}| >= tau_x, compared
@@ -283,7 +304,17 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         }
     }
 
-    // ---- kept rows to their padded list positions (x as bf16/fp16 bits) ----
+    float xscale = 1.0f, xunscale = 1.0f;   // 2^s and 2^-s (bf16 x to fp16)
+    if constexpr (kScaleX) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int w = 0; w < kMaxBlockWaves; ++w) m = max(m, wmax[w]);
+        const int sx = min(100, max(-100, 141 - (int)(m >> 7)));   // 2^14 <= max |x| 2^s < 2^15
+        xscale = __uint_as_float((uint32_t)(127 + sx) << 23);
+        xunscale = __uint_as_float((uint32_t)(127 - sx) << 23);
+    }
+
+    // ---- kept rows to their padded list positions (x as 16-bit bits) ----
     // A kept input's position: its entry's first position plus its rank in
     // the entry (a lane count).
     const int swid = wave_id();
@@ -313,7 +344,11 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         }
 #pragma unroll
         for (int r = 0; r < C; ++r) {
-            if (pos[r] >= 0) xs_sh[b * cap + pos[r]] = b < nb ? xv[r] : (uint16_t)0;
+            if (pos[r] >= 0) {
+                uint16_t v = b < nb ? xv[r] : (uint16_t)0;
+                if constexpr (kScaleX) v = float_to_f16_rne(bf16_lo(v) * xscale);   // exact
+                xs_sh[b * cap + pos[r]] = v;
+            }
         }
     }
     for (int g = tid; g < ng; g += kBlock) {
@@ -381,7 +416,8 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                     const float sg = f16_bits_to_float((e & 1) ? (sw[e >> 1] >> 16) : (sw[e >> 1] & 0xFFFFu));
 #pragma unroll
                     for (int b = 0; b < NB; ++b) {
-                        tot[b][z * 8 + e] = fmaf(sg, acc[b][z * 8 + e] - off * xs[b], tot[b][z * 8 + e]);
+                        const float offe = kHx ? kInt4HBias[e & 1] : off;
+                        tot[b][z * 8 + e] = fmaf(sg, acc[b][z * 8 + e] - offe * xs[b], tot[b][z * 8 + e]);
                         acc[b][z * 8 + e] = 0.0f;
                     }
                 }
@@ -420,12 +456,19 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
                         if constexpr (kHoistX) xp = p < pb ? xpre[u] : 0u;
                         else xp = p < pb ? xs32[b * (cap / 2) + p] : 0u;
                         pair_accumulate<DT, QB, CPL, (NB <= 2)>(wa[u], wb[u], xp, acc[b]);
-                        xs[b] = dot2<DT>(xp, Int4Magic<DT>::one, xs[b]);
+                        if constexpr (kHx) xs[b] = dot2<kF16>(xp, Int4Magic<kF16>::one, xs[b]);
+                        else xs[b] = dot2<DT>(xp, Int4Magic<DT>::one, xs[b]);
                     }
                 }
             }
         }
         flush();
+    }
+    if constexpr (kHx) {   // high-nibble columns / 16, and 2^-s: exact powers of two
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < CPL; ++e) tot[b][e] *= kInt4HScale[e & 1] * xunscale;
     }
 
     // ---- combine lane groups, then waves, in a fixed order ----

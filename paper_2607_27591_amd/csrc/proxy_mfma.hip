@@ -126,24 +126,31 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         }
     } else {
         // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
-        // x is read XQ rows at a time so their loads are in flight together.
-        constexpr int XQ = C <= 8 ? 4 : 2;
+        // x is read XQ rows at a time, two rows' 16-bit values per register,
+        // so a round's loads are in flight together (XQ * C = 64 values in 32
+        // registers per thread: one round trip for 16 rows of d <= 4096; two
+        // rows at a time for d > 8192, where registers are short).
+        constexpr int XQ = C <= 8 ? 64 / C : 2;
         uint32_t key[C];
     #pragma unroll
         for (int r = 0; r < C; ++r) key[r] = 0u;
         for (int b0 = 0; b0 < B_all; b0 += XQ) {
-            uint32_t raw[XQ][C];
+            uint32_t raw[XQ / 2][C];
     #pragma unroll
-            for (int q = 0; q < XQ; ++q) {
-                const uint16_t *xb = x_all + (size_t)min(b0 + q, B_all - 1) * d;
-    #pragma unroll
-                for (int r = 0; r < C; ++r) raw[q][r] = xb[min(r * kBlock + tid, d - 1)];
-            }
-    #pragma unroll
-            for (int q = 0; q < XQ; ++q)
+            for (int q = 0; q < XQ / 2; ++q) {
+                const uint16_t *xa = x_all + (size_t)min(b0 + 2 * q, B_all - 1) * d;
+                const uint16_t *xc = x_all + (size_t)min(b0 + 2 * q + 1, B_all - 1) * d;
     #pragma unroll
                 for (int r = 0; r < C; ++r)
-                    if (r * kBlock + tid < d) key[r] = max(key[r], raw[q][r] & 0x7FFFu);
+                    raw[q][r] = (uint32_t)xa[min(r * kBlock + tid, d - 1)] |
+                                ((uint32_t)xc[min(r * kBlock + tid, d - 1)] << 16);
+            }
+    #pragma unroll
+            for (int q = 0; q < XQ / 2; ++q)
+    #pragma unroll
+                for (int r = 0; r < C; ++r)
+                    if (r * kBlock + tid < d)
+                        key[r] = max(key[r], max(raw[q][r] & 0x7FFFu, (raw[q][r] >> 16) & 0x7FFFu));
         }
         uint64_t sel = 0;
         if (sel_rule.tau_mode) {
@@ -180,17 +187,19 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
             if (s) rows_sh[pos[r]] = (uint16_t)i;
         }
         // Only the nb real batch rows are stored: the stream feeds zeros for the
-        // others.
-        for (int b0 = 0; b0 < nb; b0 += XQ) {
-            uint16_t xv[XQ][C];
+        // others.  XL rows at a time, only the kept inputs loaded, all of a
+        // round in flight together.
+        constexpr int XL = 32 / C;   // rows per round: 32 values per thread
+        for (int b0 = 0; b0 < nb; b0 += XL) {
+            uint16_t xv[XL][C];
     #pragma unroll
-            for (int q = 0; q < XQ; ++q) {
+            for (int q = 0; q < XL; ++q) {
                 const uint16_t *xb = x_all + (size_t)(row0 + min(b0 + q, nb - 1)) * d;
     #pragma unroll
-                for (int r = 0; r < C; ++r) xv[q][r] = xb[min(r * kBlock + tid, d - 1)];
+                for (int r = 0; r < C; ++r) xv[q][r] = pos[r] >= 0 ? xb[min(r * kBlock + tid, d - 1)] : (uint16_t)0;
             }
     #pragma unroll
-            for (int q = 0; q < XQ; ++q)
+            for (int q = 0; q < XL; ++q)
                 if (b0 + q < nb)
     #pragma unroll
                     for (int r = 0; r < C; ++r)
@@ -204,14 +213,26 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         }
     }
     __syncthreads();   // the kept rows are in place: pads copy the group's last one
-    for (int g = tid; g < ng; g += kBlock) {
+    // Pads, one thread per (group, pad slot): at most 15 per group.
+    for (int it = tid; it < ng * kMfmaBlock; it += kBlock) {
+        const int g = it / kMfmaBlock, j = it % kMfmaBlock;
         const int cnt = gsel0[g + 1] - gsel0[g];
-        const int p0 = gstart[g], p1 = gstart[g + 1];
-        for (int p = p0 + cnt; p < p1; ++p) {   // p1 > p0 + cnt only when cnt > 0
+        const int p0 = gstart[g], p = p0 + cnt + j;
+        if (p < gstart[g + 1]) {   // a pad only when cnt > 0
             rows_sh[p] = rows_sh[p0 + cnt - 1];
             for (int b = 0; b < nb; ++b) xs_sh[b * cap + p] = 0;
         }
-        for (int kb = p0 / kMfmaBlock; kb < p1 / kMfmaBlock; ++kb) kbg_sh[kb] = (uint16_t)g;
+    }
+    // The group of every 16-row block: the last g with gstart[g] <= its start.
+    const int nkb_all = gstart[ng] / kMfmaBlock;
+    for (int kb = tid; kb < nkb_all; kb += kBlock) {
+        int lo = 0, hi = ng - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (gstart[mid] <= kb * kMfmaBlock) lo = mid;
+            else hi = mid - 1;
+        }
+        kbg_sh[kb] = (uint16_t)lo;
     }
     __syncthreads();
     if (tile == 0 && in_mask && list_mode != kListRead) {   // stores overlap the stream

@@ -902,9 +902,7 @@ static hipError_t launch_stage2_c(const void *x, int nb, int d, int f, const Sta
         if (scores && f <= 12 * kBlock) return S2C(12);
     }
     if (!scores || f <= 16 * kBlock) return S2C(16);
-    if constexpr (WQ == 16) {   // measured slower than 32 with INT4 weights
-        if (f <= 28 * kBlock) return S2C(28);
-    }
+    if (f <= 28 * kBlock) return S2C(28);
     if (f <= 32 * kBlock) return S2C(32);
     return S2C(64);
 #undef S2C

@@ -340,6 +340,8 @@ def w4_leg(args, cfg, w, proxy, xs, n_x, B, ws, y, mask, k_in, k_ff, timed, prox
     combination Sec. 5.1 leaves to future work), and the dense FFN on the
     same INT4 weights as its baseline; same cold protocol and decode vectors."""
     q = prox.pack_w4(w, cfg.group)
+    if prox.workspace_bytes(cfg.d_model, cfg.d_ff, B, w4=True) > ws.numel():
+        ws = prox.new_workspace(cfg.d_model, cfg.d_ff, B, ws.device, w4=True)
 
     def sparse(i, events=None):
         prox.ffn_sparse_w4(q, proxy, xs[i % n_x], k_in, k_ff, y=y, mask=mask, ws=ws,

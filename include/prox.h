@@ -134,8 +134,13 @@ prox_status prox_unpack_proxy(const prox_proxy *p, int d_model, int d_ff, int8_t
                               uint16_t *scales_gate, int8_t *codes_up, uint16_t *scales_up,
                               hipStream_t stream);
 
-/* Workspace bytes needed by prox_ffn_sparse / prox_ffn_dense for this shape
- * and batch; 0 if unsupported.  The workspace needs no initialisation. */
+/* Workspace bytes needed by prox_ffn_sparse / prox_ffn_dense (16-bit
+ * weights) for this shape and batch; 0 if unsupported.  The workspace needs
+ * no initialisation.  It holds the proxy scores, the kept-channel list and
+ * the partial y of Stage 2: one row set per Stage 2 workgroup (256), or, for
+ * more than 8 batch rows at d_model >= 4096, per kept-channel group of the
+ * matrix-core down projection (64) plus s of the kept channels.  INT4 base
+ * weights always take the 256 row sets: see prox_w4_workspace_bytes. */
 size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
 
 /*
@@ -299,22 +304,29 @@ prox_status prox_pack_w4(const prox_weights *w, const prox_w4_weights *q, hipStr
 prox_status prox_unpack_w4(const prox_w4_weights *q, int matrix, int8_t *codes,
                            uint16_t *scales, hipStream_t stream);
 
+/* Workspace bytes needed by the calls on INT4 base weights (the *_w4 calls)
+ * for this shape and batch (>= prox_workspace_bytes; equal up to 8 rows);
+ * 0 if unsupported.  No initialisation needed. */
+size_t prox_w4_workspace_bytes(int d_model, int d_ff, int batch);
+
 /* The dense FFN on the INT4 weights (every channel; the W4 baseline).
- * x, y, batch, ws, ws_bytes as prox_ffn_dense. */
+ * x, y, batch as prox_ffn_dense; ws: ws_bytes >= prox_w4_workspace_bytes(),
+ * 256-byte aligned. */
 prox_status prox_ffn_dense_w4(const prox_w4_weights *q, const void *x, int batch, void *y,
                               void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* The sparse decode step of prox_ffn_sparse with Stage 2 on the INT4 weights.
  * p is the proxy of the same FFN.  events: NULL, or PROX_SPARSE_STAGES + 1
- * caller-created events recorded as in prox_ffn_sparse_staged.  Other
- * arguments as prox_ffn_sparse. */
+ * caller-created events recorded as in prox_ffn_sparse_staged.  ws: ws_bytes
+ * >= prox_w4_workspace_bytes().  Other arguments as prox_ffn_sparse. */
 prox_status prox_ffn_sparse_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
                                int batch, int k_in, int k_ff, void *y, uint8_t *mask,
                                uint8_t *in_mask, float *scores, void *ws, size_t ws_bytes,
                                hipEvent_t *events, hipStream_t stream);
 
 /* The threshold-mode step of prox_ffn_sparse_tau with Stage 2 on the INT4
- * weights.  Arguments as prox_ffn_sparse_tau, with q in place of w. */
+ * weights.  Arguments as prox_ffn_sparse_tau, with q in place of w and ws_bytes
+ * >= prox_w4_workspace_bytes(). */
 prox_status prox_ffn_sparse_tau_w4(const prox_w4_weights *q, const prox_proxy *p, const void *x,
                                    int batch, float tau_x, float tau_s, void *y, uint8_t *mask,
                                    uint8_t *in_mask, float *scores, int32_t *counts, void *ws,

@@ -86,8 +86,8 @@ struct Ws {
     int32_t *klist;
 };
 
-Ws carve(void *ws, int d, int f, int batch) {
-    const WsLayout L(d, f, batch);
+Ws carve(void *ws, int d, int f, int batch, int wq) {
+    const WsLayout L(d, f, batch, wq);
     char *b = static_cast<char *>(ws);
     Ws w;
     w.scores = reinterpret_cast<float *>(b + L.scores);
@@ -202,7 +202,7 @@ prox_status sparse_run(const Model &m, const prox_proxy *p, const void *x, int b
                        float *scores, void *ws, hipEvent_t *events, hipStream_t stream) {
     const int d = m.d, f = m.f;
     const int qbits = qbits_of(p->fmt);
-    const Ws W = carve(ws, d, f, batch);
+    const Ws W = carve(ws, d, f, batch, m.s2.wq);
     const int dt = m.dtype;
     if (events) PROX_TRY(hipEventRecord(events[0], stream));
     // Several batch rows with an INT4 proxy: the matrix-core kernel, which
@@ -239,7 +239,7 @@ prox_status sparse_impl(const Model &m, const prox_proxy *p, const void *x, int 
     prox_status st = sparse_check(m, p, x, batch, k_in, k_ff, rules, y, mask, scores, events);
     if (st != PROX_OK) return st;
     if (!ws || !aligned(ws, 256)) return PROX_ERR_INVALID;
-    if (ws_bytes < WsLayout(m.d, m.f, batch).total) return PROX_ERR_WORKSPACE;
+    if (ws_bytes < WsLayout(m.d, m.f, batch, m.s2.wq).total) return PROX_ERR_WORKSPACE;
     return sparse_run(m, p, x, batch, k_in, k_ff, rules, y, mask, in_mask, scores, ws, events,
                       stream);
 }
@@ -249,8 +249,8 @@ prox_status dense_impl(const Model &m, const void *x, int batch, void *y, void *
     if (!x || !y || !ws) return PROX_ERR_INVALID;
     if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 256)) return PROX_ERR_INVALID;
     if (batch < 1 || batch > PROX_MAX_BATCH) return PROX_ERR_INVALID;
-    if (ws_bytes < WsLayout(m.d, m.f, batch).total) return PROX_ERR_WORKSPACE;
-    const Ws W = carve(ws, m.d, m.f, batch);
+    if (ws_bytes < WsLayout(m.d, m.f, batch, m.s2.wq).total) return PROX_ERR_WORKSPACE;
+    const Ws W = carve(ws, m.d, m.f, batch, m.s2.wq);
     return stage2_and_reduce(m, x, batch, m.f, nullptr, nullptr, nullptr, y, W,
                              Select{0, 0.0f, nullptr}, nullptr, stream);
 }
@@ -322,7 +322,12 @@ size_t prox_proxy_bytes(int d_model, int d_ff, prox_qfmt fmt, int group) {
 
 size_t prox_workspace_bytes(int d_model, int d_ff, int batch) {
     if (!shape_ok(d_model, d_ff) || batch < 1 || batch > PROX_MAX_BATCH) return 0;
-    return WsLayout(d_model, d_ff, batch).total;
+    return WsLayout(d_model, d_ff, batch, 16).total;
+}
+
+size_t prox_w4_workspace_bytes(int d_model, int d_ff, int batch) {
+    if (!shape_ok(d_model, d_ff) || batch < 1 || batch > PROX_MAX_BATCH) return 0;
+    return WsLayout(d_model, d_ff, batch, 4).total;
 }
 
 prox_status prox_pack_proxy(const prox_weights *w, prox_proxy *p, hipStream_t stream) {
@@ -378,7 +383,7 @@ prox_status prox_ffn_sparse_noalloc(const prox_weights *w, const prox_proxy *p, 
     const Rules rules{0, 0.0f, 0.0f, nullptr};
     st = sparse_check(m, p, x, batch, k_in, k_ff, rules, y, mask, scores, nullptr);
     if (st != PROX_OK) return st;
-    if (WsLayout(m.d, m.f, batch).total > PROX_NOALLOC_SCRATCH_BYTES) return PROX_ERR_WORKSPACE;
+    if (WsLayout(m.d, m.f, batch, m.s2.wq).total > PROX_NOALLOC_SCRATCH_BYTES) return PROX_ERR_WORKSPACE;
     void *ws = nullptr;
     st = scratch_of_current_device(&ws);
     if (st != PROX_OK) return st;

@@ -132,19 +132,29 @@ struct Select {
 // ---------------------------------------------------------------------------
 // Workspace (no initialisation needed)
 // ---------------------------------------------------------------------------
-// scores: the proxy scores (fp32, f padded to 128); ypart: per-workgroup
-// partial y rows of Stage 2; sbuf (more than kStage2MaxNB rows only): s of
-// the kept channels in kept-list order, [f][kStage2MfmaRows] fp32.
+// scores: the proxy scores (fp32, f padded to 128); ypart: the partial y rows
+// of Stage 2, one set per Stage 2 workgroup (kStage2MaxWGs), or per
+// kept-channel group of the matrix-core down projection (kStage2DownGroups)
+// when a batch of more than kStage2MaxNB rows of 16-bit weights takes that
+// path; sbuf (that path only): s of the kept channels in kept-list order,
+// [f][kStage2MfmaRows] fp32.  wq: 16 for 16-bit weights, 4 for INT4 ones.
+// Shapes the matrix-core Stage 2 takes: 16-bit weights, d_model >= 4096.
+__host__ __device__ inline bool stage2_mfma_shape(int d, int wq) { return wq == 16 && d >= 4096; }
+__host__ __device__ inline bool ws_mfma_path(int d, int batch, int wq) {
+    return batch > kStage2MaxNB && stage2_mfma_shape(d, wq);
+}
 struct WsLayout {
     size_t scores, klist, ypart, sbuf, total;
-    __host__ __device__ WsLayout(int d, int f, int batch) {
+    __host__ __device__ WsLayout(int d, int f, int batch, int wq) {
         const int f_pad = (f + 127) / 128 * 128;
+        const bool mfma = ws_mfma_path(d, batch, wq);
+        const size_t groups = mfma ? kStage2DownGroups : kStage2MaxWGs;
         size_t o = 0;
         scores = o; o = align_up(o + (size_t)f_pad * 4, 256);
         klist = o; o = align_up(o + (size_t)(f + 1) * 4, 256);   // kept channels, then their count
-        ypart = o; o = align_up(o + (size_t)kStage2MaxWGs * ypart_rows(batch) * d * 4, 256);
+        ypart = o; o = align_up(o + groups * ypart_rows(batch) * d * 4, 256);
         sbuf = o;
-        if (batch > kStage2MaxNB) o = align_up(o + (size_t)f * kStage2MfmaRows * 4, 256);
+        if (mfma) o = align_up(o + (size_t)f * kStage2MfmaRows * 4, 256);
         total = o;
     }
 };

@@ -586,7 +586,7 @@ size_t stage2_mfma_lds_bytes() {
     return (size_t)kS2mRed * 16 > kSelHistF32Bytes ? (size_t)kS2mRed * 16 : kSelHistF32Bytes;
 }
 
-bool stage2_mfma_ok(int d, int wq) { return wq == 16 && d >= 4 * kBlock; }
+bool stage2_mfma_ok(int d, int wq) { return stage2_mfma_shape(d, wq); }
 
 template <int DT, int C>
 __global__ __launch_bounds__(kBlock) void stage2_mfma_kernel(

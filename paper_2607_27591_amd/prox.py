@@ -72,6 +72,8 @@ def lib() -> ctypes.CDLL:
         L.prox_unpack_proxy.argtypes = [PP, I, I, P, P, P, P, P]
         L.prox_workspace_bytes.argtypes = [I, I, I]
         L.prox_workspace_bytes.restype = S
+        L.prox_w4_workspace_bytes.argtypes = [I, I, I]
+        L.prox_w4_workspace_bytes.restype = S
         L.prox_stage1_mfma_rows.argtypes = [I, I, I, I, I]
         L.prox_stage1_mfma_rows.restype = I
         L.prox_stage2_rows.argtypes = [I, I, I, I]
@@ -204,14 +206,16 @@ def stage2_rows(d_model: int, d_ff: int, w4: bool, batch: int) -> int:
     return int(lib().prox_stage2_rows(d_model, d_ff, int(w4), batch))
 
 
-def workspace_bytes(d_model: int, d_ff: int, batch: int) -> int:
-    return int(lib().prox_workspace_bytes(d_model, d_ff, batch))
+def workspace_bytes(d_model: int, d_ff: int, batch: int, w4: bool = False) -> int:
+    """prox_workspace_bytes, or prox_w4_workspace_bytes for INT4 base weights."""
+    f = lib().prox_w4_workspace_bytes if w4 else lib().prox_workspace_bytes
+    return int(f(d_model, d_ff, batch))
 
 
-def new_workspace(d_model: int, d_ff: int, batch: int, device="cuda") -> torch.Tensor:
-    n = workspace_bytes(d_model, d_ff, batch)
+def new_workspace(d_model: int, d_ff: int, batch: int, device="cuda", w4: bool = False) -> torch.Tensor:
+    n = workspace_bytes(d_model, d_ff, batch, w4)
     if n == 0:
-        raise ProxError(2, "prox_workspace_bytes")
+        raise ProxError(2, "prox_w4_workspace_bytes" if w4 else "prox_workspace_bytes")
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -414,7 +418,7 @@ def ffn_dense_w4(q: W4Weights, x: torch.Tensor, y: Optional[torch.Tensor] = None
     x = _as_batch_w4(x, q)
     B = x.shape[0]
     y = torch.empty_like(x) if y is None else _dev_tensor(y, "y", q.dtype)
-    ws = new_workspace(q.d_model, q.d_ff, B, x.device) if ws is None else ws
+    ws = new_workspace(q.d_model, q.d_ff, B, x.device, w4=True) if ws is None else ws
     qs = q.struct()
     _check(lib().prox_ffn_dense_w4(ctypes.byref(qs), _ptr(x), B, _ptr(y), _ptr(ws), ws.numel(),
                                    _stream(x.device)), "prox_ffn_dense_w4")
@@ -438,7 +442,7 @@ def ffn_sparse_w4(q: W4Weights, p: Proxy, x: torch.Tensor, k_in: int, k_ff: int,
         _dev_tensor(in_mask, "in_mask", torch.uint8)
     if scores is not None:
         _dev_tensor(scores, "scores", torch.float32)
-    ws = new_workspace(q.d_model, q.d_ff, B, dev) if ws is None else ws
+    ws = new_workspace(q.d_model, q.d_ff, B, dev, w4=True) if ws is None else ws
     arr = None
     if events is not None:
         if len(events) != SPARSE_STAGES + 1:
@@ -470,7 +474,7 @@ def ffn_sparse_tau_w4(q: W4Weights, p: Proxy, x: torch.Tensor, tau_x: float, tau
         _dev_tensor(in_mask, "in_mask", torch.uint8)
     if scores is not None:
         _dev_tensor(scores, "scores", torch.float32)
-    ws = new_workspace(q.d_model, q.d_ff, B, dev) if ws is None else ws
+    ws = new_workspace(q.d_model, q.d_ff, B, dev, w4=True) if ws is None else ws
     qs, pst = q.struct(), p.struct()
     _check(lib().prox_ffn_sparse_tau_w4(ctypes.byref(qs), ctypes.byref(pst), _ptr(x), B,
                                         float(tau_x), float(tau_s), _ptr(y), _ptr(mask),

@@ -103,6 +103,15 @@ def test_sizes():
     assert prox.workspace_bytes(4096, 65537, 1) == 0
     assert prox.workspace_bytes(4096, 12288, 16) > prox.workspace_bytes(4096, 12288, 1)
     assert prox.workspace_bytes(4096, 12288, 64) > prox.workspace_bytes(4096, 12288, 16)
+    # Partial y sized by path: up to 8 rows both weight kinds take one row set
+    # per Stage 2 workgroup; past 8 rows at d_model >= 4096 the 16-bit path
+    # keeps 64 groups (plus s), INT4 weights still 256 workgroups.
+    for B in (1, 4, 8):
+        assert prox.workspace_bytes(8192, 28672, B) == prox.workspace_bytes(8192, 28672, B, w4=True)
+    assert prox.workspace_bytes(4096, 14336, 16) < prox.workspace_bytes(4096, 14336, 16, w4=True)
+    assert prox.workspace_bytes(1024, 3072, 16) == prox.workspace_bytes(1024, 3072, 16, w4=True)
+    assert prox.workspace_bytes(4096, 14336, 16) < 256 * 16 * 4096 * 4
+    assert prox.workspace_bytes(4096, 12288, 65, w4=True) == 0
 
 
 def test_stage1_kernel_selection():

@@ -346,13 +346,18 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
 #pragma unroll
     for (int q = 0; q < PER; ++q) red[tid + q * kBlock] = outv[q];
     __syncthreads();
+    // |act(g~) u~| of every (row, column) in parallel, then the max over rows.
+    float *sv = red + NOUT;   // [16][T]
+    for (int e = tid; e < 16 * T; e += kBlock) {
+        const int b = e / T, col = e % T;
+        sv[e] = b < nb ? fabsf(gate_act(red[b * T + col], act) * red[(16 + b) * T + col]) : 0.0f;
+    }
+    __syncthreads();
     if (tid < T) {
         const int j = tile * T + tid;
         float best = 0.0f;
-        for (int b = 0; b < nb; ++b) {
-            const float gv = red[(0 * 16 + b) * T + tid], uv = red[(1 * 16 + b) * T + tid];
-            best = fmaxf(best, fabsf(gate_act(gv, act) * uv));
-        }
+#pragma unroll
+        for (int b = 0; b < 16; ++b) best = fmaxf(best, sv[b * T + tid]);
         if (j < f) scores[j] = accumulate ? fmaxf(scores[j], best) : best;
     }
 }

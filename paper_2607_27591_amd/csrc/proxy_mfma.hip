@@ -134,8 +134,11 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         uint32_t key[C];
     #pragma unroll
         for (int r = 0; r < C; ++r) key[r] = 0u;
+        // With 4 inputs per thread one round holds all 16 rows: a single
+        // launch keeps them in registers for the list instead of reloading.
+        constexpr bool kKeepX = C == 4;
+        uint32_t raw[XQ / 2][C];
         for (int b0 = 0; b0 < B_all; b0 += XQ) {
-            uint32_t raw[XQ / 2][C];
     #pragma unroll
             for (int q = 0; q < XQ / 2; ++q) {
                 const uint16_t *xa = x_all + (size_t)min(b0 + 2 * q, B_all - 1) * d;
@@ -190,6 +193,15 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         // others.  XL rows at a time, only the kept inputs loaded, all of a
         // round in flight together.
         constexpr int XL = 32 / C;   // rows per round: 32 values per thread
+        if (kKeepX && B_all <= XQ && row0 == 0 && nb == B_all) {
+    #pragma unroll
+            for (int q = 0; q < XQ; ++q)
+                if (q < nb)
+    #pragma unroll
+                    for (int r = 0; r < C; ++r)
+                        if (pos[r] >= 0)
+                            xs_sh[q * cap + pos[r]] = (uint16_t)(raw[q / 2][r] >> (16 * (q & 1)));
+        } else
         for (int b0 = 0; b0 < nb; b0 += XL) {
             uint16_t xv[XL][C];
     #pragma unroll

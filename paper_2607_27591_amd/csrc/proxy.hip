@@ -346,7 +346,7 @@ __global__ __launch_bounds__(kBlock) void proxy_kernel(
         for (int r = 0; r < C; ++r) {
             if (pos[r] >= 0) {
                 uint16_t v = b < nb ? xv[r] : (uint16_t)0;
-                if constexpr (kScaleX) v = float_to_f16_rne(bf16_lo(v) * xscale);   // exact
+                if constexpr (kScaleX) v = float_to_f16_rne(bf16_lo(v) * xscale);   // exact above 2^-28 of the largest
                 xs_sh[b * cap + pos[r]] = v;
             }
         }

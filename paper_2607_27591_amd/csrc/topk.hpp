@@ -327,18 +327,20 @@ __device__ __forceinline__ void topk_select_u15(const uint32_t (&key)[C], int n,
     static_assert(C * NT < 65536, "a 16-bit counter holds every key");
     const int tid = threadIdx.x;
     if constexpr (C * NT <= 4096) {
-        // Few keys: bits 14..7, then 6..0, over 256- and 128-bin histograms.
-        uint32_t *h1 = hist, *h2 = hist + 256;
-        for (int i = tid; i < (256 + 128) / 4; i += NT)
+        // Few keys: bits 14..3, then 2..0, over 4096- and 8-bin histograms.
+        // The first pass takes mantissa bits as well as the exponent: keys
+        // crowd into a few exponents, and same-word LDS atomics serialise.
+        uint32_t *h1 = hist, *h2 = hist + 4096;
+        for (int i = tid; i < (4096 + 8) / 4; i += NT)
             reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
         __syncthreads();
         int kk = k, bucket;
         uint32_t d1, d2;
-        narrow_pass<NT, C, 256>(key, n, 7, 0, h1, ss, kk, bucket, d1);
-        uint32_t v = d1 << 7;
+        narrow_pass<NT, C, 4096>(key, n, 3, 0, h1, ss, kk, bucket, d1);
+        uint32_t v = d1 << 3;
         if (kk < bucket) {
-            narrow_pass<NT, C, 128>(key, n, 0, d1, h2, ss, kk, bucket, d2);
-            v = (d1 << 7) | d2;
+            narrow_pass<NT, C, 8>(key, n, 0, d1, h2, ss, kk, bucket, d2);
+            v = (d1 << 3) | d2;
             if (kk < bucket) {
                 topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
                 return;

@@ -85,6 +85,20 @@ struct Int4Magic<kF16> {
     static constexpr float offset = 1032.0f;
 };
 
+// (v & mask) | bits.  FUSED: one v_and_or_b32 (the compiler otherwise emits
+// two VOP2 instructions with literals); the asm form lengthens live ranges, so
+// it is used only where registers are not tight.
+template <bool FUSED>
+__device__ __forceinline__ uint32_t and_or(uint32_t v, uint32_t mask, uint32_t bits) {
+    if constexpr (FUSED) {
+        uint32_t r;
+        asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "s"(mask), "v"(bits));
+        return r;
+    } else {
+        return (v & mask) | bits;
+    }
+}
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 typedef short v4s __attribute__((ext_vector_type(4)));

@@ -33,20 +33,6 @@
 
 namespace prox {
 
-// (v & mask) | bits.  FUSED: one v_and_or_b32 (the compiler otherwise emits
-// two VOP2 instructions with literals); the asm form lengthens live ranges, so
-// it is used only where registers are not tight.
-template <bool FUSED>
-__device__ __forceinline__ uint32_t and_or(uint32_t v, uint32_t mask, uint32_t bits) {
-    if constexpr (FUSED) {
-        uint32_t r;
-        asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "s"(mask), "v"(bits));
-        return r;
-    } else {
-        return (v & mask) | bits;
-    }
-}
-
 // acc[c] += x_a (1024 + n_a[c]) + x_b (1024 + n_b[c]) (even c) or
 // x_a (1024 + 16 n_a[c]) + x_b (1024 + 16 n_b[c]) (odd c) for the 8 INT4
 // columns of one 32-bit word of each row, x fp16: byte k of both words side by

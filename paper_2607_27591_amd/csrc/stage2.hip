@@ -30,11 +30,18 @@ namespace prox {
 constexpr int kMaxSlice = (kMaxDFF + kStage2MaxWGs - 1) / kStage2MaxWGs;   // channels per WG
 constexpr int kMaxParts = 8;
 
-// d is cut into Q parts for the gate/up units (each part >= 2048 columns of
-// 16-bit weights, >= 8192 of INT4 codes: up to four 16-byte loads per lane).
+// d is cut into Q parts for the gate/up units: each part >= 2048 columns of
+// 16-bit weights (up to four 16-byte loads per lane and matrix); with INT4
+// codes, a power of two of equal parts of at most 4096 columns, so a part is
+// one round of two 16-byte loads per lane and matrix.
 __host__ __device__ inline int gateup_parts(int d, int nbt, int wq) {
     if (nbt > 2) return 1;
-    int q = d / (wq == 4 ? 8192 : 2048);
+    if (wq == 4) {
+        int q = 1;
+        while (q * 4096 < d && q < kMaxParts) q *= 2;
+        return q;
+    }
+    const int q = d / 2048;
     return q < 1 ? 1 : (q > kMaxParts ? kMaxParts : q);
 }
 
@@ -48,9 +55,9 @@ __host__ __device__ inline int stage2_down_groups(int d, int nbt) {
 }
 
 // Dynamic LDS ahead of s: x (when staged; with INT4 weights as permuted
-// pairs plus the sum of every 32 inputs) or the down reduction buffer.
+// pairs plus two sums per 32 inputs) or the down reduction buffer.
 __host__ __device__ inline size_t stage2_head_bytes(int d, int nbt, int wq) {
-    const size_t xbytes = x_in_lds(d, nbt) ? (size_t)nbt * d * 2 + (wq == 4 ? (size_t)nbt * (d / 32) * 4 : 0)
+    const size_t xbytes = x_in_lds(d, nbt) ? (size_t)nbt * d * 2 + (wq == 4 ? (size_t)nbt * (d / 32) * 8 : 0)
                                            : 0;
     const size_t red = stage2_down_groups(d, nbt) > 1 ? (size_t)(d / 8) * nbt * 8 * 4 : 0;
     return xbytes > red ? xbytes : red;
@@ -235,13 +242,15 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     if constexpr (!kEarlyX) load_x();
 
     uint16_t *xs = reinterpret_cast<uint16_t *>(dyn);
-    float *xsum = dyn + (size_t)NB * d / 2;   // INT4: [NB][d / 32] sums of x
+    float2 *xsum = reinterpret_cast<float2 *>(dyn + (size_t)NB * d / 2);   // INT4: [NB][d / 32]
     if constexpr (WQ == 4) {
         // x as pairs (x_{8m+k}, x_{8m+k+4}), k = 0..3, one uint4 per 8
-        // inputs: nibble k of a code word and nibble k + 4 sit in the low and
-        // high halves of (word >> 4k) & 0x000F000F, so one dot2 takes both.
-        // The sum of every 32 inputs: 8 per lane in order, then the four
-        // lanes of a 32-input run (consecutive threads) as (s0 + s1) + (s2 + s3).
+        // inputs: nibble k of a code word and nibble k + 4 sit in the two
+        // halves of the word at the same bit offsets, so one dot2 takes both.
+        // Per 32 inputs, the sums of x over the even-k pairs (the low halves
+        // of the input words) and the odd-k pairs (the high halves): 4 per
+        // lane in order, then the four lanes of a 32-input run (consecutive
+        // threads) as (s0 + s1) + (s2 + s3).
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
             const int e = k * kBlock + tid;
@@ -251,15 +260,17 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                     __builtin_amdgcn_perm(v.z, v.x, 0x05040100u), __builtin_amdgcn_perm(v.z, v.x, 0x07060302u),
                     __builtin_amdgcn_perm(v.w, v.y, 0x05040100u), __builtin_amdgcn_perm(v.w, v.y, 0x07060302u));
             const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
-            float sum = 0.0f;
+            float se = 0.0f, so = 0.0f;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                sum += lo_to_float<DT>(vw[q]);
-                sum += hi_to_float<DT>(vw[q]);
+                se += lo_to_float<DT>(vw[q]);
+                so += hi_to_float<DT>(vw[q]);
             }
-            sum += dpp_move<kDppXor1>(sum);
-            sum += dpp_move<kDppXor2>(sum);
-            if (e < NB * nvec && (tid & 3) == 0) xsum[e / 4] = sum;
+            se += dpp_move<kDppXor1>(se);
+            so += dpp_move<kDppXor1>(so);
+            se += dpp_move<kDppXor2>(se);
+            so += dpp_move<kDppXor2>(so);
+            if (e < NB * nvec && (tid & 3) == 0) xsum[e / 4] = make_float2(se, so);
         }
     } else if (xl) {
 #pragma unroll
@@ -275,66 +286,104 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const int Q = gateup_parts(d, NB, WQ);
     float *s_sh = dyn + align_up(stage2_head_bytes(d, NB, WQ), 16) / 4;   // [slice][NB]
     if constexpr (WQ == 4) {
-        // 16-byte code vectors (32 inputs, inside one group) per row.  Per
-        // vector and batch row: t = sum x_i (M + n_i) by dot2, then the group
-        // scale times (t - (M + 8) * sum x_i) into the row's total.
+        // 16-byte code vectors (32 inputs, inside one group) per row.  Each
+        // code word's nibbles go under the exponent of the magic constant M
+        // in pairs (k, k + 4): the even-k pairs from the low nibble of a byte
+        // (value M + n), the odd-k pairs from its high nibble, moved only to
+        // the top of the 16-bit mantissa (M + 8n for bf16 after one shift,
+        // M + 16n in place for fp16).  Per vector and batch row the dot2 sums
+        // t_e, t_o then give sum x (n - 8) = (t_e - B_e X_e) + (t_o - B_o X_o) / s
+        // with the even and odd x sums X_e, X_o, and the group scale
+        // multiplies that into the row's total.
         constexpr uint32_t M = Int4Magic<DT>::pair;
-        constexpr float off = Int4Magic<DT>::offset;
+        constexpr bool kBf = DT == kBF16;
+        constexpr uint32_t kOddMask = kBf ? 0x00780078u : 0x00F000F0u;
+        constexpr int kOddShift = kBf ? 1 : 0;
+        constexpr float kBiasE = kBf ? 136.0f : 1032.0f;                   // M + 8
+        constexpr float kBiasO = kBf ? 128.0f + 64.0f : 1024.0f + 128.0f;  // M + 8 s
+        constexpr float kInvO = kBf ? 0.125f : 0.0625f;                     // 1 / s
         const int ng = d / wt.group;
         const int nv4 = d / 32;
-        const int qv = nv4 / Q;
+        // Scale index of vector v: v / (group / 32) by a multiply (exact for
+        // v < 2^16).
+        const uint32_t smagic = 0xFFFFFFFFu / (uint32_t)(wt.group / 32) + 1u;
         const uint4 *xs4 = reinterpret_cast<const uint4 *>(xs);
-        constexpr int U = NB <= 2 ? 4 : 2;   // vectors in flight per lane and matrix
-        for (int unit = wid; unit < n * Q; unit += kMaxBlockWaves) {
-            const int t = unit / Q, q = unit % Q;
+        constexpr int U = 2;   // vectors per lane and matrix in one round
+        // One round of a unit: the codes and group scales of U vectors of
+        // both rows.
+        struct Round {
+            uint4 g[U], u[U];
+            uint16_t sg[U], su[U];
+        };
+        // Q is a power of two here: unit = t Q + q by shifts.
+        const int lq = __builtin_ctz((unsigned)Q);
+        auto part = [&](int q, int &v_begin, int &v_end) {
+            v_begin = (q * nv4) >> lq;
+            v_end = ((q + 1) * nv4) >> lq;
+        };
+        // The loads are issued unconditionally (lanes past the part read its
+        // last vector, whose data consume skips), so the compiler can wait
+        // for exactly the loads of the round it consumes while the next
+        // round's are in flight.
+        auto issue = [&](int unit, int v0, Round &R) {
+            const int t = unit >> lq, q = unit & (Q - 1);
             const int j = sm.list[t];
             const uint4 *rg = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(wt.wg) + (size_t)j * (d / 2));
             const uint4 *ru = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(wt.wu) + (size_t)j * (d / 2));
             const uint16_t *sgr = wt.sg + (size_t)j * ng, *sur = wt.su + (size_t)j * ng;
-            const int v_begin = q * qv, v_end = (q == Q - 1) ? nv4 : v_begin + qv;
-            float ag[NB], au[NB];
+            int v_begin, v_end;
+            part(q, v_begin, v_end);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) ag[b] = au[b] = 0.0f;
-            for (int v0 = v_begin + lane; v0 < v_end; v0 += kWave * U) {
-                uint4 gv[U], uv[U];
-                uint16_t gsb[U], usb[U];
+            for (int u = 0; u < U; ++u) {
+                const int vv = min(v_begin + v0 + u * kWave, v_end - 1);
+                R.g[u] = load_stream16(rg + vv);
+                R.u[u] = load_stream16(ru + vv);
+                const int si = (int)__umulhi((uint32_t)vv, smagic);
+                R.sg[u] = sgr[si];
+                R.su[u] = sur[si];
+            }
+        };
+        // Branch-free as well: a lane past the part computes on the part's
+        // last vector with scale 0.
+        auto consume = [&](int unit, int v0, const Round &R, float (&ag)[NB], float (&au)[NB]) {
+            int v_begin, v_end;
+            part(unit & (Q - 1), v_begin, v_end);
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int vv = v0 + u * kWave;
-                    if (vv < v_end) {
-                        gv[u] = load_stream16(rg + vv);
-                        uv[u] = load_stream16(ru + vv);
-                        gsb[u] = sgr[vv * 32 / wt.group];
-                        usb[u] = sur[vv * 32 / wt.group];
-                    }
-                }
+            for (int u = 0; u < U; ++u) {
+                const bool in = v_begin + v0 + u * kWave < v_end;
+                const int vv = min(v_begin + v0 + u * kWave, v_end - 1);
+                {
+                    const float scg = in ? f16_bits_to_float(R.sg[u]) : 0.0f;
+                    const float scu = in ? f16_bits_to_float(R.su[u]) : 0.0f;
+                    const uint32_t cgw[4] = {R.g[u].x, R.g[u].y, R.g[u].z, R.g[u].w};
+                    const uint32_t cuw[4] = {R.u[u].x, R.u[u].y, R.u[u].z, R.u[u].w};
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int vv = v0 + u * kWave;
-                    if (vv < v_end) {
-                        const float scg = f16_bits_to_float(gsb[u]), scu = f16_bits_to_float(usb[u]);
-                        const uint32_t cgw[4] = {gv[u].x, gv[u].y, gv[u].z, gv[u].w};
-                        const uint32_t cuw[4] = {uv[u].x, uv[u].y, uv[u].z, uv[u].w};
+                    for (int b = 0; b < NB; ++b) {
+                        float tge = 0.0f, tgo = 0.0f, tue = 0.0f, tuo = 0.0f;
 #pragma unroll
-                        for (int b = 0; b < NB; ++b) {
-                            float tg = 0.0f, tu = 0.0f;
-#pragma unroll
-                            for (int w4 = 0; w4 < 4; ++w4) {
-                                const uint4 P = xs4[(size_t)b * nvec + vv * 4 + w4];
-                                const uint32_t pk[4] = {P.x, P.y, P.z, P.w};
-#pragma unroll
-                                for (int k = 0; k < 4; ++k) {
-                                    tg = dot2<DT>(pk[k], ((cgw[w4] >> (4 * k)) & 0x000F000Fu) | M, tg);
-                                    tu = dot2<DT>(pk[k], ((cuw[w4] >> (4 * k)) & 0x000F000Fu) | M, tu);
-                                }
-                            }
-                            const float xv = xsum[b * nv4 + vv];
-                            ag[b] = fmaf(scg, tg - off * xv, ag[b]);
-                            au[b] = fmaf(scu, tu - off * xv, au[b]);
+                        for (int w4 = 0; w4 < 4; ++w4) {
+                            const uint4 P = xs4[(size_t)b * nvec + vv * 4 + w4];
+                            const uint32_t g8 = cgw[w4] >> 8, u8 = cuw[w4] >> 8;
+                            tge = dot2<DT>(P.x, and_or<true>(cgw[w4], 0x000F000Fu, M), tge);
+                            tue = dot2<DT>(P.x, and_or<true>(cuw[w4], 0x000F000Fu, M), tue);
+                            tgo = dot2<DT>(P.y, and_or<true>(cgw[w4] >> kOddShift, kOddMask, M), tgo);
+                            tuo = dot2<DT>(P.y, and_or<true>(cuw[w4] >> kOddShift, kOddMask, M), tuo);
+                            tge = dot2<DT>(P.z, and_or<true>(g8, 0x000F000Fu, M), tge);
+                            tue = dot2<DT>(P.z, and_or<true>(u8, 0x000F000Fu, M), tue);
+                            tgo = dot2<DT>(P.w, and_or<true>(g8 >> kOddShift, kOddMask, M), tgo);
+                            tuo = dot2<DT>(P.w, and_or<true>(u8 >> kOddShift, kOddMask, M), tuo);
                         }
+                        const float2 xv = xsum[b * nv4 + vv];
+                        const float ge = tge - kBiasE * xv.x, go = tgo - kBiasO * xv.y;
+                        const float ue = tue - kBiasE * xv.x, uo = tuo - kBiasO * xv.y;
+                        ag[b] = fmaf(scg, fmaf(go, kInvO, ge), ag[b]);
+                        au[b] = fmaf(scu, fmaf(uo, kInvO, ue), au[b]);
                     }
                 }
             }
+        };
+        auto finish = [&](int unit, float (&ag)[NB], float (&au)[NB]) {
+            const int t = unit >> lq, q = unit & (Q - 1);
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const float gs = wave_sum(ag[b]);
@@ -347,6 +396,56 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                         sm.gu[((t * Q + q) * 2 + b) * 2 + 1] = us;
                     }
                 }
+            }
+        };
+        const int nunits = n * Q;
+        if constexpr (NB == 1) {
+            // A unit is one round (a part holds at most U * kWave vectors).
+            // The wave's next unit is loaded before this one is computed, so
+            // its load latency hides behind this unit's dequant and dot
+            // products; two register sets take turns.
+            auto run = [&](int unit, const Round &cur, Round &nxt) {
+                // The last unit of the wave loads itself again (unused).
+                issue(min(unit + kMaxBlockWaves, nunits - 1), lane, nxt);
+                float ag[NB], au[NB];
+#pragma unroll
+                for (int b = 0; b < NB; ++b) ag[b] = au[b] = 0.0f;
+                consume(unit, lane, cur, ag, au);
+                finish(unit, ag, au);
+            };
+            Round ra, rb;
+            // Nothing loaded before the loop is left in flight, so the waits
+            // inside it only ever count the loop's own loads.
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            // The loop leaves at either half, so its back edge is taken only
+            // after both register sets were consumed in turn (unit and count
+            // wave-uniform, so the branches are scalar).
+            int unit = __builtin_amdgcn_readfirstlane(wid);
+            const int nu = __builtin_amdgcn_readfirstlane(nunits);
+            if (unit < nu) {
+                issue(unit, lane, ra);
+                while (true) {
+                    run(unit, ra, rb);
+                    unit += kMaxBlockWaves;
+                    if (unit >= nu) break;
+                    run(unit, rb, ra);
+                    unit += kMaxBlockWaves;
+                    if (unit >= nu) break;
+                }
+            }
+        } else {
+            for (int unit = wid; unit < nunits; unit += kMaxBlockWaves) {
+                int v_begin, v_end;
+                part(unit & (Q - 1), v_begin, v_end);
+                float ag[NB], au[NB];
+#pragma unroll
+                for (int b = 0; b < NB; ++b) ag[b] = au[b] = 0.0f;
+                for (int v0 = lane; v_begin + v0 < v_end; v0 += kWave * U) {
+                    Round R;
+                    issue(unit, v0, R);
+                    consume(unit, v0, R, ag, au);
+                }
+                finish(unit, ag, au);
             }
         }
     } else {
@@ -441,56 +540,93 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
             for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
         if constexpr (WQ == 4) {
             // 8 columns per thread: one 32-bit code word and the scale of
-            // their group per channel row.  The codes n = q + 8 are split into
-            // bytes and converted one byte each; sum_j s_j sigma_j (n - 8) is
-            // taken as sum_j s_j sigma_j n minus 8 sum_j s_j sigma_j, once.
+            // their group per channel row.  The word's nibbles go under the
+            // exponent of 1024.0 in fp16 pairs (columns e, e + 4): even e
+            // from the low nibble of a byte (1024 + n), odd e from its high
+            // nibble in place (1024 + 16 n); mixed-precision FMAs take each
+            // half straight into the fp32 sums.  With S = sum_j s_j sigma_j,
+            // sum_j s_j sigma_j (n - 8) is acc - 1032 S (even e) or
+            // (acc - 1152 S) / 16 (odd e).
             const int ng = d / wt.group;
-            constexpr int UD4 = NB <= 2 ? 16 : 8;   // rows in flight: 4 bytes each
+            constexpr uint32_t M16 = Int4Magic<kF16>::pair;
+            constexpr int UD4 = NB == 1 ? 8 : 4;   // rows per round: 4 bytes each
+            const uint32_t smagic = 0xFFFFFFFFu / (uint32_t)(wt.group / 8) + 1u;
+            const int si = (int)__umulhi((uint32_t)cg, smagic);   // cg * 8 / group
             float ssum[NB];
 #pragma unroll
             for (int b = 0; b < NB; ++b) ssum[b] = 0.0f;
-            if (active) {
-                for (int t0 = gi; t0 < n; t0 += G * UD4) {
-                    uint32_t cw[UD4];
-                    uint16_t sb[UD4];
+            // One round: UD4 rows of this thread group's channels, loaded
+            // unconditionally (rows past n repeat the last one and get s = 0)
+            // so the loop can keep the next round in flight while it
+            // computes this one.
+            struct DRound {
+                uint32_t cw[UD4];
+                uint16_t sb[UD4];
+            };
+            auto issue = [&](int t0, DRound &R) {
 #pragma unroll
-                    for (int u = 0; u < UD4; ++u) {
-                        const int t = t0 + u * G;
-                        if (t < n) {
-                            const int j = sm.list[t];
-                            cw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(
-                                static_cast<const uint8_t *>(wt.wd) + (size_t)j * (d / 2) + cg * 4));
-                            sb[u] = wt.sd[(size_t)j * ng + cg * 8 / wt.group];
-                        }
-                    }
+                for (int u = 0; u < UD4; ++u) {
+                    const int j = sm.list[min(t0 + u * G, n - 1)];
+                    R.cw[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(
+                        static_cast<const uint8_t *>(wt.wd) + (size_t)j * (d / 2) + cg * 4));
+                    R.sb[u] = wt.sd[(size_t)j * ng + si];
+                }
+            };
+            auto consume = [&](int t0, const DRound &R) {
 #pragma unroll
-                    for (int u = 0; u < UD4; ++u) {
-                        const int t = t0 + u * G;
-                        if (t < n) {
-                            const float sc = f16_bits_to_float(sb[u]);
-                            const uint32_t lo = cw[u] & 0x0F0F0F0Fu;          // columns 0, 2, 4, 6
-                            const uint32_t hi = (cw[u] >> 4) & 0x0F0F0F0Fu;   // columns 1, 3, 5, 7
-                            float wf[8];
+                for (int u = 0; u < UD4; ++u) {
+                    const int t = t0 + u * G;
+                    const float sc = t < n ? f16_bits_to_float(R.sb[u]) : 0.0f;
+                    const int tc = min(t, n - 1);
+                    const uint32_t w8 = R.cw[u] >> 8;
+                    const uint32_t h[4] = {and_or<true>(R.cw[u], 0x000F000Fu, M16),
+                                           and_or<true>(R.cw[u], 0x00F000F0u, M16),
+                                           and_or<true>(w8, 0x000F000Fu, M16),
+                                           and_or<true>(w8, 0x00F000F0u, M16)};
 #pragma unroll
-                            for (int k = 0; k < 4; ++k) {
-                                wf[2 * k] = (float)((lo >> (8 * k)) & 0xFFu);
-                                wf[2 * k + 1] = (float)((hi >> (8 * k)) & 0xFFu);
-                            }
+                    for (int b = 0; b < NB; ++b) {
+                        const float sv = s_sh[tc * NB + b] * sc;
+                        ssum[b] += sv;
 #pragma unroll
-                            for (int b = 0; b < NB; ++b) {
-                                const float sv = s_sh[t * NB + b] * sc;
-                                ssum[b] += sv;
-#pragma unroll
-                                for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
-                            }
+                        for (int e = 0; e < 4; ++e) {
+                            acc[b][e] = fmaf(sv, lo_to_float<kF16>(h[e]), acc[b][e]);
+                            acc[b][e + 4] = fmaf(sv, hi_to_float<kF16>(h[e]), acc[b][e + 4]);
                         }
                     }
                 }
+            };
+            // The loop leaves at either half, so its back edge follows the
+            // use of both register sets.
+            auto rounds = [&](int t0) {
+                const int step = G * UD4;
+                DRound ra, rb;
+                issue(t0, ra);
+                while (true) {
+                    issue(min(t0 + step, n - 1), rb);
+                    consume(t0, ra);
+                    t0 += step;
+                    if (t0 >= n) break;
+                    issue(min(t0 + step, n - 1), ra);
+                    consume(t0, rb);
+                    t0 += step;
+                    if (t0 >= n) break;
+                }
+            };
+            if (active && n > 0) {
+                // Thread groups of whole waves (the usual case) take scalar
+                // round starts, and the loop's branches are uniform.
+                if (stride % kWave == 0) rounds(__builtin_amdgcn_readfirstlane(gi));
+                else rounds(gi);
             }
+            // acc[b][e] is column 8 cg + e: columns e < 4 from the low halves
+            // of the fp16 pairs, e + 4 from the high halves; odd columns came
+            // from high nibbles.
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(-8.0f, ssum[b], acc[b][e]);
+                for (int e = 0; e < 8; ++e)
+                    acc[b][e] = (e & 1) ? (acc[b][e] - 1152.0f * ssum[b]) * 0.0625f
+                                        : acc[b][e] - 1032.0f * ssum[b];
         } else if (active) {
             for (int t0 = gi; t0 < n; t0 += G * UD) {
                 uint4 wv[UD];

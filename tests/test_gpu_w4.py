@@ -27,6 +27,10 @@ CASES = {
                                             ff_frac=0.3, sigma_w=0.02), prox.SILU),
     "f16_w4_512x700_b2": (W.small_config(d=512, f=700, batch=2, seed=72, dtype=W.DT_F16,
                                          ff_frac=0.5), prox.SILU),
+    # d / 8 = 80 output columns per thread group: the down projection's
+    # thread groups do not line up with waves.
+    "bf16_w4_640x900_b1": (W.small_config(d=640, f=900, batch=1, seed=78, in_frac=0.4,
+                                          ff_frac=0.3, sigma_w=0.02), prox.SILU),
     "bf16_w4_g256_2048x3000_b5": (W.small_config(d=2048, f=3000, batch=5, seed=73, group=256,
                                                  sigma_w=0.02), prox.SILU),
     "bf16_w4_geglu_1024x900_b3": (W.small_config(d=1024, f=900, batch=3, seed=74,

@@ -373,9 +373,10 @@ __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n,
                                                 uint32_t *hist, SelScratch &ss,
                                                 TopKOrder<C> &ord) {
     const int tid = threadIdx.x;
-    if constexpr (C * NT <= 8192) {
-        // Few keys: bits 30..20, 19..9 and 8..0 over 2048-, 2048- and 512-bin
-        // histograms.
+    if constexpr (C * NT <= 16384) {
+        // Up to 16 keys per thread: bits 30..20, 19..9 and 8..0 over 2048-,
+        // 2048- and 512-bin histograms (small histograms to clear and scan
+        // cost less than the fewer passes of the wide one).
         uint32_t *g1 = hist, *g2 = hist + 2048, *g3 = hist + 4096;
         for (int i = tid; i < (4096 + 512) / 4; i += NT)
             reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);

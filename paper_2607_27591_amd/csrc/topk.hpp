@@ -10,13 +10,12 @@
 //
 // The k-th largest key is found with histograms in LDS: one pass over all
 // 2^15 values of a 16-bit magnitude (two 16-bit counters per word), or, for
-// fp32 scores, passes over bits 30..17 of every key, then bits 16..6 and 5..0
-// of the keys that match the digits found so far, ending as soon as the found
-// bin is wholly in the top k.  Small blocks (at most 4096 items of 16-bit
-// keys, 8192 scores) take narrow passes instead, whose scans are cheaper than
-// the items they add: 8 + 7 bits for 16-bit keys, 11 + 11 + 9 for scores.  A
-// pass is one round of LDS atomics and a block-wide scan of the bin counts
-// from the top.  Ties at the k-th key are
+// fp32 scores, three passes over 12 + 11 + 8 bits (11 + 11 + 9 up to 16 keys
+// per thread), the later ones over the keys that match the digits found so
+// far, ending as soon as the found bin is wholly in the top k.  Small blocks
+// of 16-bit keys (at most 4096 items) take two passes of 12 + 3 bits instead,
+// whose scans are cheaper than the items they add.  A pass is one round of
+// LDS atomics and a block-wide scan of the bin counts from the top.  Ties at the k-th key are
 // cut by index: of the keys equal to it, those up to the index of the needed
 // one are in.  The selection then costs one or two compares per item: each
 // wave keeps the ballots of its rows (TopKOrder), and one scan of their
@@ -51,9 +50,9 @@ __host__ __device__ constexpr uint32_t hist_pad(uint32_t w) { return w + (w >> 4
 constexpr int kSelPadWords = 16384 + 1024;
 
 // LDS words of the histograms: 2^15 packed 16-bit counters (input keys), or
-// 2^14 + 2^11 + 2^6 counters (the three digits of a score key).
+// at most 2^12 + 2^11 + 2^8 counters (the three digits of a score key).
 constexpr int kSelHistU16Words = kSelPadWords;
-constexpr int kSelHistF32Words = kSelPadWords + 2048 + 64;
+constexpr int kSelHistF32Words = 4096 + 2048 + 256;
 constexpr size_t kSelHistU16Bytes = (size_t)kSelHistU16Words * 4;
 constexpr size_t kSelHistF32Bytes = (size_t)kSelHistF32Words * 4;
 
@@ -363,94 +362,42 @@ __device__ __forceinline__ void topk_select_u15(const uint32_t (&key)[C], int n,
     else topk_table<NT, C>(key, n, v, ord);
 }
 
-// Top k (1 <= k <= n) of non-negative fp32 keys (bit 31 clear): bits 30..17
-// of every key, then bits 16..6 and 5..0 of the keys matching the digits
-// found so far (a wave row with none of them is skipped whole), until the
-// found bin is wholly in the top k; ties at the k-th key are cut by index.
-// hist: kSelHistF32Words words of LDS.  Fills ord.
+// Top k (1 <= k <= n) of non-negative fp32 keys (bit 31 clear) in three
+// radix passes over small histograms: bits 30..20, 19..9 and 8..0 (2048, 2048
+// and 512 bins) up to 16 keys per thread, else bits 30..19, 18..8 and 7..0
+// (4096, 2048 and 256 bins); the later passes count only the keys matching
+// the digits found so far, and stop once the found bin is wholly in the top
+// k.  Ties at the k-th key are cut by index.  hist: kSelHistF32Words words of
+// LDS.  Fills ord.
 template <int NT, int C>
 __device__ __forceinline__ void topk_select_f32(const uint32_t (&key)[C], int n, int k,
                                                 uint32_t *hist, SelScratch &ss,
                                                 TopKOrder<C> &ord) {
     const int tid = threadIdx.x;
-    if constexpr (C * NT <= 16384) {
-        // Up to 16 keys per thread: bits 30..20, 19..9 and 8..0 over 2048-,
-        // 2048- and 512-bin histograms (small histograms to clear and scan
-        // cost less than the fewer passes of the wide one).
-        uint32_t *g1 = hist, *g2 = hist + 2048, *g3 = hist + 4096;
-        for (int i = tid; i < (4096 + 512) / 4; i += NT)
-            reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
-        __syncthreads();
-        int kk = k, bucket;
-        uint32_t d1, d2, d3;
-        narrow_pass<NT, C, 2048>(key, n, 20, 0, g1, ss, kk, bucket, d1);
-        uint32_t v = d1 << 20;
-        if (kk < bucket) {
-            narrow_pass<NT, C, 2048>(key, n, 9, d1, g2, ss, kk, bucket, d2);
-            v = (d1 << 20) | (d2 << 9);
-            if (kk < bucket) {
-                narrow_pass<NT, C, 512>(key, n, 0, (d1 << 11) | d2, g3, ss, kk, bucket, d3);
-                v |= d3;
-                if (kk < bucket) {
-                    topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
-                    return;
-                }
-            }
-        }
-        topk_table<NT, C>(key, n, v, ord);
-        return;
-    }
-    uint32_t *h1 = hist, *h2 = hist + kSelPadWords, *h3 = h2 + 2048;
-    for (int i = tid; i < kSelHistF32Words / 4; i += NT)
+    constexpr int L1 = C * NT <= 16384 ? 11 : 12, L2 = 11, L3 = 31 - L1 - L2;
+    constexpr int S1 = 31 - L1, S2 = S1 - L2;
+    static_assert((1 << L1) + (1 << L2) + (1 << L3) <= kSelHistF32Words, "histograms fit");
+    uint32_t *g1 = hist, *g2 = hist + (1 << L1), *g3 = g2 + (1 << L2);
+    for (int i = tid; i < ((1 << L1) + (1 << L2) + (1 << L3)) / 4; i += NT)
         reinterpret_cast<uint4 *>(hist)[i] = make_uint4(0, 0, 0, 0);
     __syncthreads();
-#pragma unroll
-    for (int r = 0; r < C; ++r) atomicAdd(&h1[hist_pad(key[r] >> 17)], 1u);
-    if (tid == 0 && n < C * NT) atomicSub(&h1[0], (uint32_t)(C * NT - n));   // the items past n
-    __syncthreads();
-    uint32_t d1;
-    int kk, bucket;
-    find_digit<16384, false>(h1, k, ss, d1, kk, bucket);
-    uint32_t thr = d1 << 17;
+    int kk = k, bucket;
+    uint32_t d1, d2, d3;
+    narrow_pass<NT, C, (1 << L1)>(key, n, S1, 0, g1, ss, kk, bucket, d1);
+    uint32_t v = d1 << S1;
     if (kk < bucket) {
-        // Items past n hold key 0: their lanes are masked only when the bin
-        // found so far is the one holding 0.
-        const uint32_t lo = d1 << 17;
-        if (lo == 0) {
-#pragma unroll
-            for (int r = 0; r < C; ++r)
-                if (key[r] < (1u << 17) && r * NT + tid < n) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
-        } else {
-#pragma unroll
-            for (int r = 0; r < C; ++r)
-                if (key[r] - lo < (1u << 17)) atomicAdd(&h2[(key[r] >> 6) & 2047u], 1u);
-        }
-        __syncthreads();
-        uint32_t d2;
-        find_digit<2048, false>(h2, kk, ss, d2, kk, bucket);
-        uint32_t v = lo | (d2 << 6);
+        narrow_pass<NT, C, (1 << L2)>(key, n, S2, d1, g2, ss, kk, bucket, d2);
+        v = (d1 << S1) | (d2 << S2);
         if (kk < bucket) {
-            if (v == 0) {
-#pragma unroll
-                for (int r = 0; r < C; ++r)
-                    if (key[r] < 64u && r * NT + tid < n) atomicAdd(&h3[key[r] & 63u], 1u);
-            } else {
-#pragma unroll
-                for (int r = 0; r < C; ++r)
-                    if (key[r] - v < 64u) atomicAdd(&h3[key[r] & 63u], 1u);
-            }
-            __syncthreads();
-            uint32_t d3;
-            find_digit<64, false>(h3, kk, ss, d3, kk, bucket);
+            narrow_pass<NT, C, (1 << L3)>(key, n, 0, (d1 << L2) | d2, g3, ss, kk, bucket, d3);
             v |= d3;
-        }
-        thr = v;
-        if (kk < bucket) {
-            topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
-            return;
+            if (kk < bucket) {
+                topk_table_cut<NT, C>(key, n, v, kk, hist, ord);
+                return;
+            }
         }
     }
-    topk_table<NT, C>(key, n, thr, ord);
+    topk_table<NT, C>(key, n, v, ord);
 }
 
 // Ascending position (among the selected) of this thread's selected item r.

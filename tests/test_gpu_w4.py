@@ -31,6 +31,10 @@ CASES = {
     # thread groups do not line up with waves.
     "bf16_w4_640x900_b1": (W.small_config(d=640, f=900, batch=1, seed=78, in_frac=0.4,
                                           ff_frac=0.3, sigma_w=0.02), prox.SILU),
+    # fp16 at one batch row (the one-row gate/up loop with fp16 codes), and
+    # d / 8 = 144 columns per down thread group.
+    "f16_w4_1152x800_b1": (W.small_config(d=1152, f=800, batch=1, seed=79, dtype=W.DT_F16,
+                                          in_frac=0.4, ff_frac=0.3), prox.SILU),
     "bf16_w4_g256_2048x3000_b5": (W.small_config(d=2048, f=3000, batch=5, seed=73, group=256,
                                                  sigma_w=0.02), prox.SILU),
     "bf16_w4_geglu_1024x900_b3": (W.small_config(d=1024, f=900, batch=3, seed=74,

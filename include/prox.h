@@ -147,8 +147,8 @@ size_t prox_workspace_bytes(int d_model, int d_ff, int batch);
  * Which Stage-1 kernel a sparse call takes (for inspection and tests): the
  * batch rows one launch of the matrix-core kernel covers for this shape, or 0
  * when Stage 1 runs on the dot-product kernel (an INT8 or unquantised proxy,
- * fewer than five batch rows, or a kept-input list too long for the LDS, or
- * an unsupported shape).  k_in is the kept-input count; the threshold entry
+ * fewer than three batch rows up to d_model 4096 or fewer than five above, a
+ * kept-input list too long for the LDS, or an unsupported shape).  k_in is the kept-input count; the threshold entry
  * point sizes its list for k_in = d_model.  Host only, no HIP calls.  The two
  * kernels compute the same proxy in a different fp32 summation order.
  */

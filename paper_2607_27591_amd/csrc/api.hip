@@ -158,7 +158,7 @@ prox_status stage2_and_reduce(const Model &m, const void *x, int batch, int k_ff
 
 // Batch rows per matrix-core Stage-1 launch, or 0 for the dot-product kernel.
 int stage1_mfma_rows(int d, int qbits, int group, int batch, int k_in) {
-    return qbits == 4 && batch >= kProxyMfmaMinRows ? proxy_mfma_rows(d, group, k_in) : 0;
+    return qbits == 4 && batch >= proxy_mfma_min_rows(d) ? proxy_mfma_rows(d, group, k_in) : 0;
 }
 
 // The selection of each stage: counts (k_in, k_ff) or thresholds.

@@ -53,7 +53,9 @@ hipError_t launch_proxy_mfma(int dtype, const void *x_all, int B_all, int row0, 
                              int f, int group, int k_in, const void *blob, uint8_t *in_mask,
                              float *scores, int accumulate, Select sel, int act, int32_t *klist,
                              int list_mode, hipStream_t stream);
-constexpr int kProxyMfmaMinRows = 5;   // batch rows from which Stage 1 uses the matrix cores
+// Batch rows from which Stage 1 uses the matrix cores: 3 up to d_model 4096,
+// 5 above (where its 2-byte code loads keep too few bytes in flight).
+inline int proxy_mfma_min_rows(int d) { return d <= 4096 ? 3 : 5; }
 
 // The three matrices of Stage 2: channel-major 16-bit rows (wq == 16), or
 // INT4 codes with fp16 scales per (channel, group along d), laid out as

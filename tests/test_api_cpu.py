@@ -115,14 +115,17 @@ def test_sizes():
 
 
 def test_stage1_kernel_selection():
-    # The matrix-core Stage 1 takes INT4 proxies from five batch rows on, with
-    # 16 rows per launch while the kept-row list and 16 x rows fit the LDS,
-    # then 8; otherwise (and for INT8, unquantised or bad shapes) the
-    # dot-product kernel (0).
+    # The matrix-core Stage 1 takes INT4 proxies from three batch rows on up to
+    # d_model 4096 and from five above, with 16 rows per launch while the
+    # kept-row list and 16 x rows fit the LDS, then 8; otherwise (and for
+    # INT8, unquantised or bad shapes) the dot-product kernel (0).
     rows = prox.stage1_mfma_rows
     assert rows(4096, prox.INT4, 128, 16, 2048) == 16
     assert rows(4096, prox.INT4, 128, 5, 2048) == 16
-    assert rows(4096, prox.INT4, 128, 4, 2048) == 0        # four rows: dot product
+    assert rows(4096, prox.INT4, 128, 3, 2048) == 16
+    assert rows(4096, prox.INT4, 128, 2, 2048) == 0        # two rows: dot product
+    assert rows(8192, prox.INT4, 128, 4, 3277) == 0        # four rows at 8192: dot product
+    assert rows(8192, prox.INT4, 128, 5, 3277) == 8
     assert rows(4096, prox.INT4, 128, 12, 4096) == 8       # threshold-mode list
     assert rows(8192, prox.INT4, 128, 16, 3277) == 8
     assert rows(8192, prox.INT4, 128, 16, 8192) == 0       # list too long

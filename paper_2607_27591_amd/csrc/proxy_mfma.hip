@@ -37,7 +37,7 @@ constexpr int kMfmaU = 4;         // blocks in flight per wave
 
 
 // Dynamic LDS: first the input selection's histogram; then rows [cap] u16,
-// x [NX][cap] u16, block groups [cap / 16] u16; after the stream the same space holds the cross-wave partial sums
+// x [cap][NX] u16 (position-major), block groups [cap / 16] u16; after the stream the same space holds the cross-wave partial sums
 // [16 waves][64 lanes][16] f32.
 __host__ __device__ inline int mfma_list_cap(int k_in, int ng) {
     return (k_in + ng * (kMfmaBlock - 1) + kMfmaBlock - 1) / kMfmaBlock * kMfmaBlock;
@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
             const int g = (int)__umulhi((uint32_t)i, gmagic);
             const int p = gstart[g] + idx - gsel0[g];
             rows_sh[p] = (uint16_t)i;
-            for (int b = 0; b < nb; ++b) xs_sh[b * cap + p] = x_all[(size_t)(row0 + b) * d + i];
+            for (int b = 0; b < nb; ++b) xs_sh[(size_t)p * NX + b] = x_all[(size_t)(row0 + b) * d + i];
         }
     } else {
         // ---- input selection (as proxy_kernel): key = max_b |x_{b,i}| bits ----
@@ -194,13 +194,17 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         // round in flight together.
         constexpr int XL = 32 / C;   // rows per round: 32 values per thread
         if (kKeepX && B_all <= XQ && row0 == 0 && nb == B_all) {
+            // raw[q][r] already holds rows 2q and 2q + 1 side by side: NX rows
+            // of a kept input are NX / 8 16-byte stores (rows past nb hold
+            // copies, never read).
     #pragma unroll
-            for (int q = 0; q < XQ; ++q)
-                if (q < nb)
+            for (int r = 0; r < C; ++r)
+                if (pos[r] >= 0) {
+                    uint4 *dst = reinterpret_cast<uint4 *>(xs_sh + (size_t)pos[r] * NX);
     #pragma unroll
-                    for (int r = 0; r < C; ++r)
-                        if (pos[r] >= 0)
-                            xs_sh[q * cap + pos[r]] = (uint16_t)(raw[q / 2][r] >> (16 * (q & 1)));
+                    for (int h = 0; h < NX / 8; ++h)
+                        dst[h] = make_uint4(raw[4 * h][r], raw[4 * h + 1][r], raw[4 * h + 2][r], raw[4 * h + 3][r]);
+                }
         } else
         for (int b0 = 0; b0 < nb; b0 += XL) {
             uint16_t xv[XL][C];
@@ -210,12 +214,23 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
     #pragma unroll
                 for (int r = 0; r < C; ++r) xv[q][r] = pos[r] >= 0 ? xb[min(r * kBlock + tid, d - 1)] : (uint16_t)0;
             }
+            // The round's XL rows of a kept input are contiguous: one store
+            // (rows past nb hold copies, never read; b0 + XL <= NX).
     #pragma unroll
-            for (int q = 0; q < XL; ++q)
-                if (b0 + q < nb)
+            for (int r = 0; r < C; ++r)
+                if (pos[r] >= 0) {
+                    uint32_t w[XL / 2];
     #pragma unroll
-                    for (int r = 0; r < C; ++r)
-                        if (pos[r] >= 0) xs_sh[(b0 + q) * cap + pos[r]] = xv[q][r];
+                    for (int q = 0; q < XL / 2; ++q)
+                        w[q] = (uint32_t)xv[2 * q][r] | ((uint32_t)xv[2 * q + 1][r] << 16);
+                    uint16_t *dst = xs_sh + (size_t)pos[r] * NX + b0;
+                    if constexpr (XL == 8)
+                        *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+                    else if constexpr (XL == 4)
+                        *reinterpret_cast<uint2 *>(dst) = make_uint2(w[0], w[1]);
+                    else
+                        *reinterpret_cast<uint32_t *>(dst) = w[0];
+                }
         }
         if (list_mode == kListWrite && tile == 0) {   // the list for the later launches
 #pragma unroll
@@ -232,7 +247,9 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         const int p0 = gstart[g], p = p0 + cnt + j;
         if (p < gstart[g + 1]) {   // a pad only when cnt > 0
             rows_sh[p] = rows_sh[p0 + cnt - 1];
-            for (int b = 0; b < nb; ++b) xs_sh[b * cap + p] = 0;
+            uint4 *dst = reinterpret_cast<uint4 *>(xs_sh + (size_t)p * NX);
+#pragma unroll
+            for (int h = 0; h < NX / 8; ++h) dst[h] = make_uint4(0u, 0u, 0u, 0u);
         }
     }
     // The group of every 16-row block: the last g with gstart[g] <= its start.
@@ -299,7 +316,11 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
                 const int k = min(kb + u, kb1 - 1);
                 const uint2 rr = *reinterpret_cast<const uint2 *>(rows_sh + k * kMfmaBlock + lg * 4);
                 const uint32_t r4[4] = {rr.x & 0xFFFFu, rr.x >> 16, rr.y & 0xFFFFu, rr.y >> 16};
-                xa[u] = ln < nb ? *reinterpret_cast<const uint2 *>(xs_sh + ln * cap + k * kMfmaBlock + lg * 4)
+                // x of batch row ln at the block's rows 4 lg .. 4 lg + 3
+                // (position-major: NX rows per kept position).
+                const uint16_t *xq = xs_sh + (size_t)(k * kMfmaBlock + lg * 4) * NX + min(ln, NX - 1);
+                xa[u] = ln < nb ? make_uint2((uint32_t)xq[0] | ((uint32_t)xq[NX] << 16),
+                                             (uint32_t)xq[2 * NX] | ((uint32_t)xq[3 * NX] << 16))
                                 : make_uint2(0u, 0u);
                 gk[u] = kbg_sh[k];
 #pragma unroll

@@ -359,39 +359,29 @@ __global__ __launch_bounds__(kBlock) void proxy_mfma_kernel(
         *reinterpret_cast<float4 *>(red + ((size_t)(wid * kWave + lane) * 16 + c * 4)) =
             make_float4(tot[c][0], tot[c][1], tot[c][2], tot[c][3]);
     __syncthreads();
-    // Output o = ((m * 16 + b) * T + col): thread t sums outputs t, t + kBlock, ...
-    constexpr int NOUT = 2 * 16 * T;
-    constexpr int PER = NOUT / kBlock;
-    float outv[PER];
+    // Every (row b, column col): the sums of the WPG waves of the gate and of
+    // the up matrix in wave order, then |act(g~) u~|, then the max over the 16
+    // rows inside each 16-lane row of the wave (lane % 16 = b, one column).
+    const int b = tid % 16;
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const int o = tid + q * kBlock;
-        const int m = o / (16 * T), b = (o / T) % 16, col = o % T;
+    for (int q = 0; q < T / 64; ++q) {
+        const int col = tid / 16 + q * 64;
         const int hh = col / 64, cl = col % 64;
-        const int src_lane = (b / 4) * 16 + cl / 4, c = cl % 4, j = b % 4;
-        const int wbase = (hh * 2 + m) * WPG;   // the waves of this (half, matrix)
-        float s = 0.0f;
-        for (int w2 = 0; w2 < WPG; ++w2)
-            s += red[(size_t)((wbase + w2) * kWave + src_lane) * 16 + c * 4 + j];
-        outv[q] = s;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < PER; ++q) red[tid + q * kBlock] = outv[q];
-    __syncthreads();
-    // |act(g~) u~| of every (row, column) in parallel, then the max over rows.
-    float *sv = red + NOUT;   // [16][T]
-    for (int e = tid; e < 16 * T; e += kBlock) {
-        const int b = e / T, col = e % T;
-        sv[e] = b < nb ? fabsf(gate_act(red[b * T + col], act) * red[(16 + b) * T + col]) : 0.0f;
-    }
-    __syncthreads();
-    if (tid < T) {
-        const int j = tile * T + tid;
-        float best = 0.0f;
-#pragma unroll
-        for (int b = 0; b < 16; ++b) best = fmaxf(best, sv[b * T + tid]);
-        if (j < f) scores[j] = accumulate ? fmaxf(scores[j], best) : best;
+        const int src = ((b / 4) * 16 + cl / 4) * 16 + (cl % 4) * 4 + b % 4;   // lane, c, j
+        const float *rg = red + (size_t)(hh * 2 + 0) * WPG * kWave * 16 + src;
+        const float *ru = red + (size_t)(hh * 2 + 1) * WPG * kWave * 16 + src;
+        float gs = 0.0f, us = 0.0f;
+        for (int w2 = 0; w2 < WPG; ++w2) {
+            gs += rg[(size_t)w2 * kWave * 16];
+            us += ru[(size_t)w2 * kWave * 16];
+        }
+        float v = b < nb ? fabsf(gate_act(gs, act) * us) : 0.0f;
+        v = fmaxf(v, dpp_move<kDppXor1>(v));
+        v = fmaxf(v, dpp_move<kDppXor2>(v));
+        v = fmaxf(v, dpp_move<kDppRor4>(v));
+        v = fmaxf(v, dpp_move<kDppRor8>(v));
+        const int j = tile * T + col;
+        if (b == 0 && j < f) scores[j] = accumulate ? fmaxf(scores[j], v) : v;
     }
 }
 

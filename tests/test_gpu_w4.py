@@ -45,6 +45,12 @@ CASES = {
                                             sigma_w=0.01), prox.SILU),
     "bf16_w4_16384x320_b3": (W.small_config(d=16384, f=320, batch=3, seed=76, in_frac=0.3,
                                             sigma_w=0.01), prox.SILU),
+    # One batch row with the gate/up parts of the one-row loop: four parts of
+    # 4096 columns (d 16384) and four uneven ones of 3072 (d 12288).
+    "bf16_w4_16384x300_b1": (W.small_config(d=16384, f=300, batch=1, seed=80, in_frac=0.3,
+                                            sigma_w=0.01), prox.SILU),
+    "bf16_w4_12288x700_b1": (W.small_config(d=12288, f=700, batch=1, seed=81, in_frac=0.4,
+                                            sigma_w=0.01), prox.GELU),
 }
 
 

@@ -14,6 +14,30 @@ from gpu_cases import Y_TOL, check_pack, check_sparse, log, make_case, run_spars
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 
+def _ties(case, batch, tag):
+    """All-tied and equal-magnitude inputs at full size: every selection
+    breaks its ties by the lower index (App. A.6), here with d_ff score keys
+    per call (above 16384 the channel top-k takes its 12-bit first pass)."""
+    cfg = case.cfg
+    k_in, k_ff = cfg.k_in, cfg.k_ff
+    x = np.zeros((batch, cfg.d_model), np.uint16)
+    x[batch - 1, 1::2] = 0x8000   # -0 ties with +0
+    log(f"[full] {tag} zero input B={batch}")
+    out = run_sparse(case, x, k_in, k_ff)
+    assert np.flatnonzero(out.in_mask).tolist() == list(range(k_in))
+    assert np.flatnonzero(out.mask).tolist() == list(range(k_ff))
+    assert not out.scores.any()
+    assert not W.bits_to_f32(out.y, cfg.dtype).any()
+    rng = np.random.default_rng(7)
+    v = rng.choice([-0.75, 0.75], size=(batch, cfg.d_model)).astype(np.float32)
+    v[:, k_in + 5:] = 0.125       # the cut falls inside a run of equal magnitudes
+    xe = W.to_bits(v, cfg.dtype)
+    log(f"[full] {tag} equal magnitudes B={batch}")
+    out = run_sparse(case, xe, k_in, k_ff)
+    assert np.flatnonzero(out.in_mask).tolist() == list(range(k_in))
+    log(f"    {check_sparse(case, xe, k_in, k_ff, out, tag=f'{tag} equal magnitudes')}")
+
+
 def _full(name, n_vectors, dense=True):
     cfg = W.CONFIGS[name]
     log(f"[full] {name}: generating and packing")
@@ -24,6 +48,7 @@ def _full(name, n_vectors, dense=True):
         log(f"[full] {name} vector {n}")
         out = run_sparse(case, x, cfg.k_in, cfg.k_ff)
         log(f"    {check_sparse(case, x, cfg.k_in, cfg.k_ff, out, tag=f'{name}/{n}')}")
+    _ties(case, cfg.batch, name)
     if dense:
         log(f"[full] {name} dense")
         y = prox.ffn_dense(case.w, prox.from_bits(xs[0], cfg.dtype))
@@ -113,6 +138,12 @@ def test_c3_batch_sparsity_sweep(c3_case, batch, sparsity):
     log(f"[full] c3 B={batch} sparsity={sparsity} k_ff={k_ff}")
     out = run_sparse(c3_case, x, cfg.k_in, k_ff)
     log(f"    {check_sparse(c3_case, x, cfg.k_in, k_ff, out, tag=f'c3 B={batch} s={sparsity}')}")
+
+
+@pytest.mark.parametrize("batch", [4, 16])
+def test_c3_ties(c3_case, batch):
+    """Ties on the dot-product (4 rows) and matrix-core (16 rows) paths."""
+    _ties(c3_case, batch, f"c3 B={batch}")
 
 
 def test_c5_stack_teacher_forced():

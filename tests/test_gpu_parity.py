@@ -64,6 +64,13 @@ SMALL = {
                                            sigma_w=0.01),
     "f16_i4_128x65536_b2": W.small_config(d=128, f=65536, batch=2, seed=12, dtype=W.DT_F16,
                                           ff_frac=0.2),
+    # The largest batch a call takes (64 rows): four 16-row launches of each
+    # matrix-core stage, and sixteen 4-row Stage 1 plus eight 8-row Stage 2
+    # launches of the dot-product kernels.
+    "bf16_i4_4096x1000_b64": W.small_config(d=4096, f=1000, batch=64, seed=24, in_frac=0.4,
+                                            sigma_w=0.02),
+    "f16_i8_512x700_b64": W.small_config(d=512, f=700, batch=64, seed=25, dtype=W.DT_F16,
+                                         qbits=8, group=512, ff_frac=0.5),
 }
 
 

@@ -51,6 +51,9 @@ CASES = {
                                             sigma_w=0.01), prox.SILU),
     "bf16_w4_12288x700_b1": (W.small_config(d=12288, f=700, batch=1, seed=81, in_frac=0.4,
                                             sigma_w=0.01), prox.GELU),
+    # The largest batch a call takes: eight 8-row Stage 2 launches.
+    "bf16_w4_1024x600_b64": (W.small_config(d=1024, f=600, batch=64, seed=82, in_frac=0.4,
+                                            sigma_w=0.02), prox.SILU),
 }
 
 

@@ -117,6 +117,38 @@ def test_max_dff_matrix_core_stage2():
     torch.cuda.empty_cache()
 
 
+def test_max_shape_d16384_f65536():
+    """Both maxima in one call at batch 1: d_model 16384 (16 input rows per
+    thread in the proxy's selection) with d_ff 65536 (64 score keys per
+    thread in Stage 2's). Packing, sparse and dense parity, full keep equal
+    to dense bitwise, then the INT4 base-weight Stage 2 at the same shape."""
+    from test_gpu_w4 import _check_w4, _run_w4
+    cfg = W.small_config(d=16384, f=65536, batch=1, seed=26, in_frac=0.4, ff_frac=0.3,
+                         sigma_w=0.01)
+    log("[full] 16384x65536 b1: generating and packing")
+    case = make_case(cfg)
+    check_pack(case)
+    x = case.wl.x_vectors(1, 1)[0]
+    out = run_sparse(case, x, cfg.k_in, cfg.k_ff)
+    log(f"    {check_sparse(case, x, cfg.k_in, cfg.k_ff, out, tag='16384x65536')}")
+    y = prox.to_bits(prox.ffn_dense(case.w, prox.from_bits(x, cfg.dtype)))
+    torch.cuda.synchronize()
+    ref = oracle.ffn_dense(x, cfg.dtype, case.wl.w_gate, case.wl.w_up, case.wl.w_down)
+    err = y_rel_err(y, ref, cfg.dtype)
+    log(f"    dense y err {err:.3e}")
+    assert err <= Y_TOL
+    full = run_sparse(case, x, cfg.d_model, cfg.d_ff)
+    assert full.mask.all() and np.array_equal(full.y, y)
+    log("[full] 16384x65536 b1: INT4 base weights")
+    q = prox.pack_w4(case.w, cfg.group)
+    w4 = oracle.quantize_w4(case.wl.w_gate, case.wl.w_up, case.wl.w_down, cfg.dtype, cfg.group)
+    stats = _check_w4(case, w4, x, cfg.k_in, cfg.k_ff, _run_w4(case, q, x, cfg.k_in, cfg.k_ff),
+                      "16384x65536 W4")
+    log(f"    W4: {stats}")
+    del case, q, w4
+    torch.cuda.empty_cache()
+
+
 @pytest.fixture(scope="module")
 def c3_case():
     cfg = W.CONFIGS["c3_4096x14336_bf16"]

@@ -156,13 +156,11 @@ def test_w4_zero_input(case):
     assert not W.bits_to_f32(y, cfg.dtype).any()
 
 
-def test_w4_threshold_mode(case):
-    # Thresholds in place of counts (prox_ffn_sparse_tau_w4): the masks follow
-    # the rule exactly on the GPU's own values, y is the oracle's W4 Stage 2 on
-    # the GPU's mask.
-    c, q, w4 = case
+def _check_w4_tau(c, q, w4, x_bits):
+    """Thresholds in place of counts (prox_ffn_sparse_tau_w4): the masks follow
+    the rule exactly on the GPU's own values, y is the oracle's W4 Stage 2 on
+    the GPU's mask."""
     cfg = c.cfg
-    x_bits = c.wl.x_vectors(1, cfg.batch)[0]
     tau_x, tau_s = quantile_taus(c, x_bits)
     x = prox.from_bits(np.atleast_2d(x_bits), cfg.dtype)
     in_mask = torch.empty(cfg.d_model, dtype=torch.uint8, device="cuda")
@@ -188,6 +186,11 @@ def test_w4_threshold_mode(case):
     assert err <= Y_TOL
 
 
+def test_w4_threshold_mode(case):
+    c, q, w4 = case
+    _check_w4_tau(c, q, w4, c.wl.x_vectors(1, c.cfg.batch)[0])
+
+
 def test_w4_c4_full_size():
     cfg = W.CONFIGS["c4_8192x28672_bf16"]
     log("[w4 full] c4: generating and packing")
@@ -197,5 +200,7 @@ def test_w4_c4_full_size():
     x = c.wl.x_vectors(1, 1)[0]
     stats = _check_w4(c, w4, x, cfg.k_in, cfg.k_ff, _run_w4(c, q, x, cfg.k_in, cfg.k_ff), "c4 W4")
     log(f"    c4 W4: {stats}")
+    log("[w4 full] c4 threshold mode")
+    _check_w4_tau(c, q, w4, x)
     del c, q
     torch.cuda.empty_cache()

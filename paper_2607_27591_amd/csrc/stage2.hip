@@ -528,7 +528,9 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     const int G = stage2_down_groups(d, NB);
     const int stride = G > 1 ? ncg : kBlock;
     const int gi = tid / stride, cgt = tid % stride;
-    float *dred = dyn;   // reuses the x area: [ncg][NB][8]
+    // Reuses the x area: [NB][8][ncg], so that the threads of a wave (adjacent
+    // column groups) store to adjacent words.
+    float *dred = dyn;
     constexpr int UD = 8;
     for (int cg0 = 0; cg0 < ncg; cg0 += stride) {
         const int cg = cg0 + cgt;
@@ -666,7 +668,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
                     for (int b = 0; b < NB; ++b)
 #pragma unroll
                         for (int e = 0; e < 8; ++e) {
-                            float *dst = &dred[(cg * NB + b) * 8 + e];
+                            float *dst = &dred[(b * 8 + e) * ncg + cg];
                             *dst = g2 == 0 ? acc[b][e] : *dst + acc[b][e];
                         }
                 }
@@ -676,7 +678,7 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) acc[b][e] = dred[(cg * NB + b) * 8 + e];
+                    for (int e = 0; e < 8; ++e) acc[b][e] = dred[(b * 8 + e) * ncg + cg];
             }
         }
         if (active && gi == 0) {

@@ -172,6 +172,19 @@ def test_c3_batch_sparsity_sweep(c3_case, batch, sparsity):
     log(f"    {check_sparse(c3_case, x, cfg.k_in, k_ff, out, tag=f'c3 B={batch} s={sparsity}')}")
 
 
+@pytest.mark.parametrize("batch", [1, 4, 16])
+def test_c3_threshold_mode(c3_case, batch):
+    """The threshold rule at full size on each Stage 1 and Stage 2 path: its
+    kept-row list holds up to d rows, so the matrix-core Stage 1 takes 8 rows
+    per launch here (two launches at 16 rows)."""
+    from test_gpu_threshold import check_tau, quantile_taus, run_tau
+    x = c3_case.wl.x_vectors(1, batch)[0]
+    tau_x, tau_s = quantile_taus(c3_case, x)
+    log(f"[full] c3 threshold mode B={batch}")
+    out, counts = run_tau(c3_case, x, tau_x, tau_s)
+    log(f"    {check_tau(c3_case, x, tau_x, tau_s, out, counts, tag=f'c3 tau B={batch}')}")
+
+
 @pytest.mark.parametrize("batch", [4, 16])
 def test_c3_ties(c3_case, batch):
     """Ties on the dot-product (4 rows) and matrix-core (16 rows) paths."""

@@ -118,10 +118,16 @@ __device__ __forceinline__ v4f mfma16(uint2 a, uint2 b, v4f c) {
                                                      __builtin_bit_cast(v4h, b), c, 0, 0, 0);
 }
 
-// 16-byte streaming load (non-temporal hint: weights are read once per call).
+// 16- and 8-byte streaming loads (non-temporal hint: weights are read once
+// per call).
 __device__ __forceinline__ uint4 load_stream16(const void *p) {
     const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
     return make_uint4(v.x, v.y, v.z, v.w);
+}
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint2 load_stream8(const void *p) {
+    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p));
+    return make_uint2(v.x, v.y);
 }
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }

@@ -525,13 +525,58 @@ __global__ __launch_bounds__(kBlock) void stage2_kernel(
     // the channels are split over G thread groups, summed through LDS in
     // group order.
     const int ncg = d / 8;
+    constexpr int UD = 8;
+    if constexpr (WQ == 16 && NB == 8) {
+        // Eight batch rows up to d = 4096: 4 columns per thread, so that every
+        // thread takes part (split channel sums would need more registers than
+        // eight rows leave).  Each column is still summed over the slice in
+        // order by one thread, as below.
+        if (ncg < kBlock && d / 4 <= kBlock) {
+            const int c4 = tid;
+            if (c4 < d / 4) {
+                float acc[NB][4];
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[b][e] = 0.0f;
+                for (int t0 = 0; t0 < n; t0 += UD) {
+                    uint2 wv[UD];
+#pragma unroll
+                    for (int u = 0; u < UD; ++u) {
+                        const int t = t0 + u;
+                        if (t < n) wv[u] = load_stream8(wd + (size_t)sm.list[t] * d + c4 * 4);
+                    }
+#pragma unroll
+                    for (int u = 0; u < UD; ++u) {
+                        const int t = t0 + u;
+                        if (t < n) {
+                            const float wf[4] = {lo_to_float<DT>(wv[u].x), hi_to_float<DT>(wv[u].x),
+                                                 lo_to_float<DT>(wv[u].y), hi_to_float<DT>(wv[u].y)};
+#pragma unroll
+                            for (int b = 0; b < NB; ++b) {
+                                const float sv = s_sh[t * NB + b];
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) acc[b][e] = fmaf(sv, wf[e], acc[b][e]);
+                            }
+                        }
+                    }
+                }
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    if (b < nb)
+                        *reinterpret_cast<float4 *>(ypart + ((size_t)blockIdx.x * ypart_stride + b) * d + c4 * 4) =
+                            make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+                }
+            }
+            return;
+        }
+    }
     const int G = stage2_down_groups(d, NB);
     const int stride = G > 1 ? ncg : kBlock;
     const int gi = tid / stride, cgt = tid % stride;
     // Reuses the x area: [NB][8][ncg], so that the threads of a wave (adjacent
     // column groups) store to adjacent words.
     float *dred = dyn;
-    constexpr int UD = 8;
     for (int cg0 = 0; cg0 < ncg; cg0 += stride) {
         const int cg = cg0 + cgt;
         const bool active = cg < ncg && gi < G;

@@ -144,6 +144,34 @@ def test_deterministic(case):
     assert np.array_equal(a.scores.view(np.uint32), b.scores.view(np.uint32))
 
 
+def _stage_events():
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(prox.SPARSE_STAGES + 1)]
+    for e in ev:
+        e.record()   # an event must exist before the library records it
+    return ev
+
+
+def check_staged(run, tag):
+    """The entry point with events between its stages (how the benchmark times
+    it) against the same call without: the same bits, and events that complete
+    in stage order."""
+    y0, m0 = run(None)
+    ev = _stage_events()
+    y1, m1 = run(ev)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1) and torch.equal(m0, m1), f"{tag}: staged call differs"
+    t = [ev[0].elapsed_time(e) for e in ev[1:]]
+    assert all(v >= 0.0 for v in t) and t == sorted(t), f"{tag}: stage events {t}"
+
+
+def test_staged_entry_point(case):
+    cfg = case.cfg
+    x = prox.from_bits(np.atleast_2d(case.wl.x_vectors(1, cfg.batch)[0]), cfg.dtype)
+    log(f"[staged] {cfg.name}")
+    check_staged(lambda ev: prox.ffn_sparse(case.w, case.proxy, x, cfg.k_in, cfg.k_ff, events=ev),
+                 cfg.name)
+
+
 # ---------------------------------------------------------------------------
 # Degenerate inputs: ties everywhere
 # ---------------------------------------------------------------------------

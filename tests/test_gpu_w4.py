@@ -191,6 +191,16 @@ def test_w4_threshold_mode(case):
     _check_w4_tau(c, q, w4, c.wl.x_vectors(1, c.cfg.batch)[0])
 
 
+def test_w4_staged_entry_point(case):
+    from test_gpu_parity import check_staged
+    c, q, w4 = case
+    cfg = c.cfg
+    x = prox.from_bits(np.atleast_2d(c.wl.x_vectors(1, cfg.batch)[0]), cfg.dtype)
+    log(f"[w4 staged] {cfg.name}")
+    check_staged(lambda ev: prox.ffn_sparse_w4(q, c.proxy, x, cfg.k_in, cfg.k_ff, events=ev),
+                 cfg.name)
+
+
 def test_w4_c4_full_size():
     cfg = W.CONFIGS["c4_8192x28672_bf16"]
     log("[w4 full] c4: generating and packing")
